@@ -1,0 +1,228 @@
+"""CPU oracle for the scheduling-decision path (test infrastructure only).
+
+Plain, slow, fp64 NumPy restatements of what each stage computes, written
+from the paper's definitions. Only ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py`` may import this module; the
+product path never does, and it imports nothing from the product package.
+
+Stages and the passages they follow:
+
+* ``round_to_bf16``   - storage of the history store / query batch: fp32
+  embeddings rounded to bf16, round-to-nearest-even (a precision choice of
+  this build; the paper does not fix one).
+* ``similarity``      - Sec. 3.1: cosine similarity of prompt embeddings;
+  for unit vectors that is the inner product (flat search, Sec. 3.1 footnote).
+* ``topk``            - Sec. 3.1: the most similar history records, taken as
+  the first ``k`` under (similarity desc, history index asc).
+* ``histogram``       - Sec. 3.1: the neighbours' output lengths form the
+  predicted distribution; records below the similarity threshold (0.8 by
+  default) get no weight, the others weigh by their similarity, and the
+  lengths are binned on log-spaced bins.
+* ``cost``            - Sec. 3.2, unified cost model: C = O^2/2 + I*O.
+* ``gittins``         - Sec. 3.3, Gittins index
+  G(D) = inf_{Delta>0} E[min(X, Delta)] / P(X <= Delta), X ~ D.
+* ``rank``            - Sec. 3.3: the smaller index is served first; ties go
+  to the lower request id.
+
+Every function here is pinned by ``-m "not gpu"`` tests against brute force,
+exact rational arithmetic, closed forms and invariants (tests/test_oracle_*.py).
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+NEG_INF = -np.inf
+
+
+# ---------------------------------------------------------------- storage
+def round_to_bf16(x) -> np.ndarray:
+    """fp32 -> bf16 bit patterns (uint16), round to nearest, ties to even.
+
+    A bf16 keeps the top 16 bits of an fp32. Rounding adds half of the
+    dropped range (0x7FFF) plus the kept part's lowest bit, so that an exact
+    half-way case rounds to the even neighbour. Inputs must be finite.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("round_to_bf16: non-finite input")
+    u = x.view(np.uint32).astype(np.uint64)
+    keep_lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = (u + np.uint64(0x7FFF) + keep_lsb) >> np.uint64(16)
+    return r.astype(np.uint16)
+
+
+def bf16_to_f64(bits) -> np.ndarray:
+    """Exact value of bf16 bit patterns as fp64."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+# ------------------------------------------------------------- similarity
+def similarity(q_bits, h_bits) -> np.ndarray:
+    """s[q, n] = sum_t Q[q, t] * H[n, t] over the stored bf16 values, in fp64.
+
+    Products of two bf16 values are exact in fp64; the sums are exact or
+    within a few fp64 ulps for the dimensions used here. No renormalisation
+    after the bf16 rounding.
+    """
+    return bf16_to_f64(q_bits) @ bf16_to_f64(h_bits).T
+
+
+# ------------------------------------------------------------------ top-k
+def topk_row(s: np.ndarray, k: int):
+    """First ``k`` history indices under (s desc, n asc), padded with (-1, -inf).
+
+    All indices whose score reaches the m-th largest value (m = min(k, N))
+    are kept before the lexicographic sort, so ties at the boundary are
+    resolved by the index rule, never by the selection routine.
+    """
+    N = s.shape[0]
+    m = min(k, N)
+    if m < N:
+        t = -np.partition(-s, m - 1)[m - 1]
+        cand = np.nonzero(s >= t)[0]
+    else:
+        cand = np.arange(N)
+    order = cand[np.lexsort((cand, -s[cand]))][:m]
+    ids = np.full(k, -1, dtype=np.int32)
+    sims = np.full(k, NEG_INF, dtype=np.float64)
+    ids[:m] = order
+    sims[:m] = s[order]
+    return ids, sims
+
+
+def topk(S: np.ndarray, k: int):
+    Q = S.shape[0]
+    ids = np.empty((Q, k), dtype=np.int32)
+    sims = np.empty((Q, k), dtype=np.float64)
+    for q in range(Q):
+        ids[q], sims[q] = topk_row(S[q], k)
+    return ids, sims
+
+
+def search(q_bits, h_bits, k: int, block: int = 128, threads: int | None = None):
+    """Similarity + top-k over the whole store, one query block at a time.
+
+    Blocking over queries only bounds memory; each row is still the plain
+    definition (full fp64 score row, then ``topk_row``).
+    """
+    Q = q_bits.shape[0]
+    hf = bf16_to_f64(h_bits)
+    ids = np.empty((Q, k), dtype=np.int32)
+    sims = np.empty((Q, k), dtype=np.float64)
+    threads = threads or os.cpu_count() or 1
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        for s0 in range(0, Q, block):
+            e0 = min(Q, s0 + block)
+            S = bf16_to_f64(q_bits[s0:e0]) @ hf.T
+            rows = list(pool.map(lambda r: topk_row(S[r], k), range(e0 - s0)))
+            for r, (i, v) in enumerate(rows):
+                ids[s0 + r], sims[s0 + r] = i, v
+    return ids, sims
+
+
+# -------------------------------------------------------------- histogram
+def bin_of(lengths, edges) -> np.ndarray:
+    """Largest b in [0, B-1] with edges[b] <= L (lengths below edges[0] -> 0)."""
+    B = edges.shape[0] - 1
+    b = np.searchsorted(edges, np.asarray(lengths, dtype=np.float64), side="right") - 1
+    return np.clip(b, 0, B - 1).astype(np.int64)
+
+
+def histogram(ids, sims, hist_len, edges, tau: float):
+    """Per-request output-length distribution from its neighbours.
+
+    counts[q, b]: neighbours (valid ids only) whose length falls in bin b.
+    mass[q, b]  : sum of w_i over those neighbours / sum of all w_i, where
+                  w_i = s_i if s_i >= tau else 0; if every w_i is 0 the mass
+                  falls back to counts / (number of valid neighbours).
+    """
+    ids = np.asarray(ids)
+    sims = np.asarray(sims, dtype=np.float64)
+    Q, _ = ids.shape
+    B = edges.shape[0] - 1
+    counts = np.zeros((Q, B), dtype=np.int32)
+    mass = np.zeros((Q, B), dtype=np.float64)
+    tau = float(np.float32(tau))
+    for q in range(Q):
+        valid = ids[q] >= 0
+        m = int(valid.sum())
+        if m == 0:
+            continue
+        b = bin_of(hist_len[ids[q][valid]], edges)
+        s = sims[q][valid]
+        w = np.where(s >= tau, s, 0.0)
+        np.add.at(counts[q], b, 1)
+        W = w.sum()
+        if W > 0:
+            np.add.at(mass[q], b, w)
+            mass[q] /= W
+        else:
+            mass[q] = counts[q] / m
+    return counts, mass
+
+
+# ------------------------------------------------------------------- cost
+def cost(prompt_len, bin_repr) -> np.ndarray:
+    """Service cost of each support point: x[q, b] = r_b^2 / 2 + I_q * r_b."""
+    I = np.asarray(prompt_len, dtype=np.float64)[:, None]
+    r = np.asarray(bin_repr, dtype=np.float64)[None, :]
+    return r * r / 2.0 + I * r
+
+
+# ----------------------------------------------------------------- index
+def gittins(mass, x):
+    """Gittins index of each row's discrete cost distribution.
+
+    With support points x_0 <= x_1 <= ... (non-decreasing, as the cost is
+    increasing in the output length) and masses p_b:
+        F_b = sum_{j<=b} p_j,  S_b = sum_{j<=b} p_j x_j,  T_b = sum_{j>b} p_j,
+        G   = min over b with F_b > 0 of (S_b + T_b x_b) / F_b.
+    For Delta in [x_b, x_{b+1}) the completion probability is F_b and the
+    expected spend S_b + T_b Delta grows with Delta, so the infimum over
+    Delta is reached at a support point. Rows with no mass get +inf (and
+    argmin -1). The index does not depend on the scale of p, so rows need
+    not sum to one. Returns (G, argmin) with argmin the smallest b at the min.
+    """
+    p = np.asarray(mass, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64)
+    if x.ndim == 1:
+        x = np.broadcast_to(x, p.shape)
+    if np.any(np.diff(x, axis=1) < 0):
+        raise ValueError("gittins: support must be non-decreasing along each row")
+    F = np.cumsum(p, axis=1)
+    S = np.cumsum(p * x, axis=1)
+    tail = np.cumsum(p[:, ::-1], axis=1)[:, ::-1]         # sum over j >= b
+    T = np.zeros_like(p)
+    T[:, :-1] = tail[:, 1:]                               # sum over j > b
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(F > 0, (S + T * x) / F, np.inf)
+    G = ratio.min(axis=1)
+    arg = np.where(np.isfinite(G), ratio.argmin(axis=1), -1).astype(np.int32)
+    return G, arg
+
+
+# ------------------------------------------------------------------ rank
+def rank(G) -> np.ndarray:
+    """Queue order: ascending index, ties to the lower request id."""
+    return np.argsort(np.asarray(G), kind="stable").astype(np.int32)
+
+
+# -------------------------------------------------------------- pipelines
+def predict(queries_f32, hist_f32, hist_len, k, tau, edges, *, block=128, threads=None):
+    """Stages storage -> similarity -> top-k -> histogram for a query batch."""
+    qb = round_to_bf16(queries_f32)
+    hb = round_to_bf16(hist_f32)
+    ids, sims = search(qb, hb, k, block=block, threads=threads)
+    counts, mass = histogram(ids, sims, hist_len, edges, tau)
+    return ids, sims, counts, mass
+
+
+def schedule(mass, prompt_len, bin_repr):
+    """Stages cost -> index -> rank."""
+    x = cost(prompt_len, bin_repr)
+    G, arg = gittins(mass, x)
+    return G, arg, rank(G)
