@@ -1,0 +1,183 @@
+/*
+ * sage.h - C ABI of the SageSched scheduling-decision path on MI355X (gfx950).
+ *
+ * For a batch of pending LLM requests the path predicts an output-length
+ * distribution from the most similar past prompts (paper Sec. 3.1), turns it
+ * into a service-cost distribution with C = O^2/2 + I*O (Sec. 3.2), computes
+ * the Gittins index of that distribution and orders the queue by it, smaller
+ * index first (Sec. 3.3).
+ *
+ * Conventions shared by every entry point:
+ *  - Every pointer is a DEVICE pointer (HBM of the current HIP device) unless
+ *    stated otherwise; all arrays are dense, row-major, and at least 16-byte
+ *    aligned. bf16 values travel as their raw 16-bit patterns (uint16_t).
+ *  - The caller owns every buffer, including the workspace. The library
+ *    allocates nothing on these paths and keeps no pointer after returning.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *    the call returns without synchronising. Arguments are validated before
+ *    anything is enqueued: a call that returns an error has enqueued nothing.
+ *    Faults while kernels run surface at the caller's synchronisation.
+ *  - Q = 0 is a valid no-op. Entry points are re-entrant on distinct streams
+ *    and distinct buffers.
+ *  - Return value: SAGE_OK or a negative sage_status; sage_last_error() gives
+ *    a human-readable detail for the calling thread.
+ */
+#ifndef SAGE_H
+#define SAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* sage_stream_t; /* == hipStream_t */
+
+enum sage_status {
+  SAGE_OK = 0,
+  SAGE_EINVAL = -1,      /* bad argument: null pointer, size or range */
+  SAGE_EWORKSPACE = -2,  /* workspace smaller than the *_workspace_bytes query */
+  SAGE_EUNSUPPORTED = -3,/* device is not gfx950 */
+  SAGE_EHIP = -4         /* a HIP runtime call failed (see sage_last_error) */
+};
+
+/* Limits checked by validation. */
+#define SAGE_MAX_K 256
+#define SAGE_MAX_BINS 4096
+
+/*
+ * sage_ingest_bf16 - store fp32 embeddings as bf16 (round to nearest, ties
+ * to even): the resident history store and the query batch are kept in bf16
+ * (the paper fixes no precision; Sec. 3.1 only needs cosine similarity).
+ *   src [n] fp32 finite values; dst [n] bf16 bit patterns. src and dst must
+ *   not overlap. n = 0 is a no-op.
+ */
+int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_stream_t stream);
+
+/*
+ * sage_predict_workspace_bytes - bytes of device workspace sage_predict needs
+ * for these sizes (holds the per-stream partial neighbour lists). Returns 0
+ * for invalid sizes.
+ */
+size_t sage_predict_workspace_bytes(int Q, int N, int d, int k, int B);
+
+/*
+ * sage_predict - semantic-aware history-based predictor (Sec. 3.1).
+ *   queries  [Q, d] bf16  prompt embeddings of the pending requests (unit norm
+ *                         expected; no renormalisation is applied)
+ *   hist_emb [N, d] bf16  history store: embeddings of past prompts
+ *   hist_len [N]   int32  their recorded output lengths (>= 1)
+ *   k                     neighbours per request, 1..SAGE_MAX_K
+ *   tau                   similarity threshold in [2^-20, 1]; neighbours
+ *                         below it get zero weight (paper default 0.8)
+ *   bin_edges [B+1] f64   strictly increasing length-bin edges; a length L
+ *                         falls in the largest b in [0, B-1] with
+ *                         edges[b] <= L (lengths below edges[0] go to bin 0)
+ *   B                     1..SAGE_MAX_BINS
+ * Outputs (row q = request q):
+ *   nbr_ids  [Q, k] int32 the k history indices with the largest similarity
+ *                         s = <query, hist_emb[n]> (fp32 accumulation of bf16
+ *                         products), ordered by (s desc, index asc); if
+ *                         N < k the tail is padded with -1
+ *   nbr_sims [Q, k] f32   their similarities (padding: -inf)
+ *   counts   [Q, B] int32 neighbours (valid ids) per length bin
+ *   mass     [Q, B] f32   similarity-weighted share per bin: sum of s_i over
+ *                         the bin's neighbours with s_i >= tau, divided by the
+ *                         same sum over all neighbours; if no neighbour reaches
+ *                         tau, counts / (number of valid neighbours)
+ *   workspace             >= sage_predict_workspace_bytes(Q, N, d, k, B) bytes
+ * Constraints: Q >= 0, N >= 1, d >= 32 and d % 32 == 0.
+ */
+int sage_predict(const uint16_t* queries, int Q,
+                 const uint16_t* hist_emb, const int32_t* hist_len, int N, int d,
+                 int k, float tau, const double* bin_edges, int B,
+                 int32_t* nbr_ids, float* nbr_sims, int32_t* counts, float* mass,
+                 void* workspace, size_t workspace_bytes, sage_stream_t stream);
+
+/*
+ * sage_histogram - the predicted output-length distribution alone (the last
+ * stage of sage_predict, Sec. 3.1), for neighbour lists obtained elsewhere.
+ *   nbr_ids [Q, k] int32 history indices; entries outside [0, N) mean "no
+ *                 neighbour" and are skipped
+ *   nbr_sims [Q, k] f32 their similarities, each below 2048 in magnitude
+ *   hist_len [N] int32 recorded output lengths of the history store
+ *   other arguments and outputs as in sage_predict.
+ * Weights are summed exactly (fixed point, 2^-43 resolution, which is exact
+ * for every fp32 weight >= tau >= 2^-20), so results do not depend on the
+ * order of the neighbours.
+ */
+int sage_histogram(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
+                   const int32_t* hist_len, int N, float tau, const double* bin_edges, int B,
+                   int32_t* counts, float* mass, sage_stream_t stream);
+
+/*
+ * sage_cost - unified compute/memory cost model (Sec. 3.2): the cost of
+ * serving request q with output length r_b is x[q, b] = r_b^2/2 + I_q * r_b,
+ * evaluated in fp64 and rounded to fp32.
+ *   prompt_len [Q] int32 (>= 0), bin_repr [B] f64 representative output
+ *   length of each bin (positive, increasing), cost [Q, B] f32 out.
+ */
+int sage_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
+              float* cost, sage_stream_t stream);
+
+/*
+ * sage_index - Gittins index of each request's cost distribution (Sec. 3.3):
+ *   G = inf over Delta > 0 of E[min(X, Delta)] / P(X <= Delta), X ~ D,
+ * where D puts mass[q, b] on cost x[q, b]. The masses need not sum to one
+ * (the index does not depend on their scale). The cost support must be
+ * non-decreasing along each row (true for sage_cost on increasing bin_repr);
+ * the index is then the minimum over the support points b with F_b > 0 of
+ * (S_b + T_b x_b) / F_b (F, S: prefix sums of p and p*x; T: mass above b).
+ *   mass [Q, B] f32, non-negative
+ *   cost [Q, B] f32, or NULL: then x is computed in fp64 from prompt_len [Q]
+ *        and bin_repr [B] as in sage_cost (fused, nothing materialised)
+ *   index [Q] f32 out: the Gittins index (+inf for a row with no mass)
+ *   argmin_bin [Q] int32 out or NULL: smallest b attaining the minimum
+ *        (-1 for a row with no mass)
+ * Accumulation is in fp64; one division per request.
+ */
+int sage_index(const float* mass, const float* cost, const int32_t* prompt_len,
+               const double* bin_repr, int Q, int B,
+               float* index, int32_t* argmin_bin, sage_stream_t stream);
+
+/* sage_rank_workspace_bytes - device workspace bytes for sage_rank(Q). */
+size_t sage_rank_workspace_bytes(int Q);
+
+/*
+ * sage_rank - queue order (Sec. 3.3: the smaller Gittins index is served
+ * first): order[0..Q) is the stable ascending argsort of index (ties keep
+ * the lower request id first; +inf sorts last). NaN is not allowed.
+ *   index [Q] f32, order [Q] int32 out (a permutation of 0..Q-1).
+ */
+int sage_rank(const float* index, int Q, int32_t* order,
+              void* workspace, size_t workspace_bytes, sage_stream_t stream);
+
+/* Static, thread-safe name of a status code. Host pointer. */
+const char* sage_status_string(int status);
+
+/* Detail of the calling thread's last failed call ("" if none). Host pointer. */
+const char* sage_last_error(void);
+
+/*
+ * Stage timer (measurement only). While a timer is attached to the calling
+ * thread, every kernel the library enqueues from that thread is bracketed by
+ * two HIP events recorded on the same stream. After synchronising, read the
+ * per-kernel totals. The timer owns its events (created once, up to
+ * `capacity` launches between resets).
+ */
+typedef struct sage_timer sage_timer;
+int sage_timer_create(int capacity, sage_timer** out);
+int sage_timer_destroy(sage_timer* t);
+int sage_timer_attach(sage_timer* t);   /* NULL detaches */
+int sage_timer_reset(sage_timer* t);
+/* Number of distinct kernel names seen since the last reset. */
+int sage_timer_count(sage_timer* t);
+/* i-th kernel: its name (host string owned by the library), launches and
+ * total elapsed milliseconds. The caller must have synchronised the streams. */
+int sage_timer_get(sage_timer* t, int i, const char** name, int* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SAGE_H */

@@ -1,0 +1,71 @@
+// Elementwise kernels: bf16 ingest of the embeddings and the materialised
+// cost support (the index scan computes the same cost inline).
+#include "sage_device.hpp"
+#include "sage_internal.hpp"
+
+namespace sage {
+namespace {
+
+// fp32 -> bf16, round to nearest, ties to even: add half of the dropped
+// 16-bit range plus the kept part's lowest bit, then truncate.
+__device__ __forceinline__ uint16_t bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__global__ void __launch_bounds__(256) ingest_bf16_kernel(const float* __restrict__ src, size_t n,
+                                                          uint16_t* __restrict__ dst) {
+  const size_t n4 = n / 4;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  const float4* s4 = reinterpret_cast<const float4*>(src);
+  ushort4* d4 = reinterpret_cast<ushort4*>(dst);
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    float4 v = s4[i];
+    d4[i] = make_ushort4(bf16_rne(v.x), bf16_rne(v.y), bf16_rne(v.z), bf16_rne(v.w));
+  }
+  for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = bf16_rne(src[i]);
+}
+
+// x[q, b] = r_b^2 / 2 + I_q * r_b in fp64, rounded once to fp32.
+__global__ void __launch_bounds__(256) cost_kernel(const int32_t* __restrict__ prompt_len, int Q,
+                                                   const double* __restrict__ repr, int B,
+                                                   float* __restrict__ cost) {
+  const size_t total = (size_t)Q * (size_t)B;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const int q = (int)(i / (size_t)B);
+    const int b = (int)(i - (size_t)q * B);
+    const double r = repr[b];
+    cost[i] = (float)fma((double)prompt_len[q], r, r * r * 0.5);
+  }
+}
+
+int grid_for(size_t work, int block, int cap = 4096) {
+  size_t g = (work + block - 1) / block;
+  if (g < 1) g = 1;
+  if (g > (size_t)cap) g = cap;
+  return (int)g;
+}
+
+}  // namespace
+
+hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  LaunchScope scope("ingest_bf16", stream);
+  hipLaunchKernelGGL(ingest_bf16_kernel, dim3(grid_for(n / 4 + 1, 256, 8192)), dim3(256), 0, stream,
+                     src, n, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B, float* cost,
+                       hipStream_t stream) {
+  if (Q == 0) return hipSuccess;
+  LaunchScope scope("cost", stream);
+  hipLaunchKernelGGL(cost_kernel, dim3(grid_for((size_t)Q * B, 256, 8192)), dim3(256), 0, stream,
+                     prompt_len, Q, bin_repr, B, cost);
+  return hipGetLastError();
+}
+
+}  // namespace sage

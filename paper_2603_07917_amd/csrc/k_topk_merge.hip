@@ -1,0 +1,82 @@
+// Merge of the per-stream neighbour lists into each request's final top-k.
+//
+// The fused similarity kernel leaves, for every request, one descending list
+// of `list_len` neighbour keys per history chunk. Here one workgroup per
+// request folds those lists together with bitonic merges in LDS: two
+// descending lists A, B of length L give C_i = max(A_i, B_{L-1-i}), a bitonic
+// sequence holding exactly the L largest keys of A and B, which log2(L)
+// half-cleaner stages sort back into descending order.
+#include "sage_device.hpp"
+#include "sage_internal.hpp"
+
+namespace sage {
+namespace {
+
+constexpr int kMergeThreads = 256;
+constexpr int kMergeKeys = 4096;   // LDS capacity in keys (32 KiB)
+
+__global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
+    const uint64_t* __restrict__ partial, int n_lists, int list_len, int k,
+    int32_t* __restrict__ ids, float* __restrict__ sims) {
+  __shared__ uint64_t slot[kMergeKeys];
+  const int q = blockIdx.x;
+  const int L = list_len;
+  const int G = kMergeKeys / L;                 // lists per LDS batch (power of two)
+  const uint64_t* src = partial + (size_t)q * n_lists * L;
+  const int t = threadIdx.x;
+
+  bool have_result = false;
+  for (int base = 0; base < n_lists || !have_result;) {
+    const int s0 = have_result ? 1 : 0;
+    const int n_load = min(G - s0, n_lists - base);
+    int n_used = s0 + n_load;
+    int n_tree = 1;
+    while (n_tree < n_used) n_tree <<= 1;
+    // Load the batch (slot 0 keeps the running result) and pad to n_tree lists.
+    for (int i = t; i < n_load * L; i += kMergeThreads) slot[s0 * L + i] = src[(size_t)base * L + i];
+    for (int i = n_used * L + t; i < n_tree * L; i += kMergeThreads) slot[i] = kPadKey;
+    __syncthreads();
+    for (int width = 1; width < n_tree; width <<= 1) {
+      const int pairs = n_tree / (2 * width);
+      // C_i = max(A_i, B_{L-1-i}) for every pair (A in slot j, B in slot j + width).
+      for (int e = t; e < pairs * L; e += kMergeThreads) {
+        const int p = e / L, i = e - p * L;
+        const int a = (2 * p) * width, b = a + width;
+        const uint64_t va = slot[a * L + i], vb = slot[b * L + (L - 1 - i)];
+        slot[a * L + i] = va > vb ? va : vb;
+      }
+      __syncthreads();
+      for (int stride = L >> 1; stride > 0; stride >>= 1) {
+        for (int e = t; e < pairs * (L >> 1); e += kMergeThreads) {
+          const int p = e / (L >> 1), r = e - p * (L >> 1);
+          const int a = (2 * p) * width;
+          const int i = (r / stride) * (2 * stride) + (r % stride);
+          uint64_t* s = slot + a * L;
+          const uint64_t x = s[i], y = s[i + stride];
+          if (y > x) { s[i] = y; s[i + stride] = x; }
+        }
+        __syncthreads();
+      }
+    }
+    have_result = true;
+    base += n_load;
+  }
+  for (int i = t; i < k; i += kMergeThreads) {
+    const uint64_t key = slot[i];
+    ids[(size_t)q * k + i] = key == kPadKey ? -1 : key_id(key);
+    sims[(size_t)q * k + i] = key == kPadKey ? -__builtin_inff() : key_sim(key);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
+                             int32_t* ids, float* sims, hipStream_t stream) {
+  if (Q == 0) return hipSuccess;
+  LaunchScope scope("topk_merge", stream);
+  hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, partial, n_lists,
+                     list_len, k, ids, sims);
+  return hipGetLastError();
+}
+
+}  // namespace sage

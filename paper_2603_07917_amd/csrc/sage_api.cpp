@@ -1,0 +1,337 @@
+// C ABI of libsage: argument validation, workspace sizing, device checks and
+// dispatch to the gfx950 kernels. Nothing here allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "sage.h"
+#include "sage_internal.hpp"
+
+#define SAGE_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local sage_timer* g_timer = nullptr;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return SAGE_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Device check, cached per device ordinal: the kernels are built for gfx950.
+int check_device() {
+  static std::mutex mu;
+  static std::vector<int> verdict;   // 0 unknown, 1 ok, -1 unsupported
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SAGE_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)verdict.size() <= dev) verdict.resize(dev + 1, 0);
+  if (verdict[dev] == 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return fail(SAGE_EHIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+    verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    if (verdict[dev] < 0)
+      return fail(SAGE_EUNSUPPORTED, "device %d is %s, the library is built for gfx950", dev,
+                  prop.gcnArchName);
+  }
+  if (verdict[dev] < 0) return fail(SAGE_EUNSUPPORTED, "device %d is not gfx950", dev);
+  return SAGE_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(SAGE_EHIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+constexpr float kMinTau = 9.5367431640625e-07f;   // 2^-20
+
+int check_bins(const double* edges, int B) {
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (!edges) return fail(SAGE_EINVAL, "bin_edges is NULL");
+  if (!aligned16(edges)) return fail(SAGE_EINVAL, "bin_edges is not 16-byte aligned");
+  return SAGE_OK;
+}
+
+int check_tau(float tau) {
+  if (!(tau >= kMinTau && tau <= 1.0f)) return fail(SAGE_EINVAL, "tau=%g outside [2^-20, 1]", (double)tau);
+  return SAGE_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ timer
+struct sage_timer {
+  int capacity = 0;
+  int used = 0;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<const char*> name;
+};
+
+namespace sage {
+LaunchScope::LaunchScope(const char* name, hipStream_t stream) : stream_(stream) {
+  sage_timer* t = g_timer;
+  if (!t || t->used >= t->capacity) return;
+  slot_ = t->used++;
+  t->name[slot_] = name;
+  (void)hipEventRecord(t->start[slot_], stream);
+}
+LaunchScope::~LaunchScope() {
+  sage_timer* t = g_timer;
+  if (slot_ < 0 || !t) return;
+  (void)hipEventRecord(t->stop[slot_], stream_);
+}
+}  // namespace sage
+
+SAGE_API int sage_timer_create(int capacity, sage_timer** out) {
+  if (!out || capacity < 1) return fail(SAGE_EINVAL, "sage_timer_create: bad arguments");
+  sage_timer* t = new sage_timer;
+  t->capacity = capacity;
+  t->start.resize(capacity);
+  t->stop.resize(capacity);
+  t->name.resize(capacity, nullptr);
+  for (int i = 0; i < capacity; ++i) {
+    hipError_t e1 = hipEventCreate(&t->start[i]);
+    hipError_t e2 = hipEventCreate(&t->stop[i]);
+    if (e1 != hipSuccess || e2 != hipSuccess) {
+      t->capacity = i;
+      sage_timer_destroy(t);
+      return fail(SAGE_EHIP, "hipEventCreate failed");
+    }
+  }
+  *out = t;
+  return ok();
+}
+
+SAGE_API int sage_timer_destroy(sage_timer* t) {
+  if (!t) return ok();
+  if (g_timer == t) g_timer = nullptr;
+  for (int i = 0; i < t->capacity; ++i) {
+    (void)hipEventDestroy(t->start[i]);
+    (void)hipEventDestroy(t->stop[i]);
+  }
+  delete t;
+  return ok();
+}
+
+SAGE_API int sage_timer_attach(sage_timer* t) {
+  g_timer = t;
+  return ok();
+}
+
+SAGE_API int sage_timer_reset(sage_timer* t) {
+  if (!t) return fail(SAGE_EINVAL, "timer is NULL");
+  t->used = 0;
+  return ok();
+}
+
+namespace {
+std::vector<const char*> timer_names(sage_timer* t) {
+  std::vector<const char*> names;
+  for (int i = 0; i < t->used; ++i) {
+    bool seen = false;
+    for (const char* n : names) seen = seen || std::strcmp(n, t->name[i]) == 0;
+    if (!seen) names.push_back(t->name[i]);
+  }
+  return names;
+}
+}  // namespace
+
+SAGE_API int sage_timer_count(sage_timer* t) {
+  if (!t) return 0;
+  return (int)timer_names(t).size();
+}
+
+SAGE_API int sage_timer_get(sage_timer* t, int i, const char** name, int* launches, double* total_ms) {
+  if (!t || !name || !launches || !total_ms) return fail(SAGE_EINVAL, "sage_timer_get: NULL argument");
+  std::vector<const char*> names = timer_names(t);
+  if (i < 0 || i >= (int)names.size()) return fail(SAGE_EINVAL, "timer index %d out of range", i);
+  int n = 0;
+  double ms = 0.0;
+  for (int j = 0; j < t->used; ++j) {
+    if (std::strcmp(t->name[j], names[i]) != 0) continue;
+    float e = 0.f;
+    hipError_t err = hipEventElapsedTime(&e, t->start[j], t->stop[j]);
+    if (err != hipSuccess) return fail(SAGE_EHIP, "hipEventElapsedTime: %s", hipGetErrorString(err));
+    ms += e;
+    ++n;
+  }
+  *name = names[i];
+  *launches = n;
+  *total_ms = ms;
+  return ok();
+}
+
+// -------------------------------------------------------------- status
+SAGE_API const char* sage_status_string(int status) {
+  switch (status) {
+    case SAGE_OK: return "SAGE_OK";
+    case SAGE_EINVAL: return "SAGE_EINVAL: invalid argument";
+    case SAGE_EWORKSPACE: return "SAGE_EWORKSPACE: workspace too small";
+    case SAGE_EUNSUPPORTED: return "SAGE_EUNSUPPORTED: device is not gfx950";
+    case SAGE_EHIP: return "SAGE_EHIP: HIP runtime error";
+    default: return "unknown sage status";
+  }
+}
+
+SAGE_API const char* sage_last_error(void) { return g_last_error.c_str(); }
+
+// ------------------------------------------------------------- ingest
+SAGE_API int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_stream_t stream) {
+  if (n == 0) return ok();
+  if (!src || !dst) return fail(SAGE_EINVAL, "sage_ingest_bf16: NULL pointer");
+  if (!aligned16(src) || !aligned16(dst)) return fail(SAGE_EINVAL, "sage_ingest_bf16: misaligned pointer");
+  const char* s0 = reinterpret_cast<const char*>(src);
+  const char* d0 = reinterpret_cast<const char*>(dst);
+  if (s0 < d0 + n * sizeof(uint16_t) && d0 < s0 + n * sizeof(float))
+    return fail(SAGE_EINVAL, "sage_ingest_bf16: src and dst overlap");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_ingest_bf16(src, n, dst, (hipStream_t)stream), "ingest_bf16 launch");
+}
+
+// ------------------------------------------------------------- predict
+namespace {
+int check_predict_sizes(int Q, int N, int d, int k, int B) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (N < 1) return fail(SAGE_EINVAL, "N=%d must be >= 1", N);
+  if (d < 32 || d % 32 != 0) return fail(SAGE_EINVAL, "d=%d must be a positive multiple of 32", d);
+  if (k < 1 || k > SAGE_MAX_K) return fail(SAGE_EINVAL, "k=%d outside [1, %d]", k, SAGE_MAX_K);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  return SAGE_OK;
+}
+}  // namespace
+
+SAGE_API size_t sage_predict_workspace_bytes(int Q, int N, int d, int k, int B) {
+  std::string keep = g_last_error;
+  if (check_predict_sizes(Q, N, d, k, B) != SAGE_OK) return 0;
+  g_last_error = keep;
+  if (Q == 0) return 0;
+  return sage::plan_sim_topk(Q, N, d, k).partial_bytes;
+}
+
+SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_emb,
+                          const int32_t* hist_len, int N, int d, int k, float tau,
+                          const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,
+                          int32_t* counts, float* mass, void* workspace, size_t workspace_bytes,
+                          sage_stream_t stream) {
+  int st = check_predict_sizes(Q, N, d, k, B);
+  if (st != SAGE_OK) return st;
+  if ((st = check_tau(tau)) != SAGE_OK) return st;
+  if (Q == 0) return ok();
+  if ((st = check_bins(bin_edges, B)) != SAGE_OK) return st;
+  const void* ptrs[] = {queries, hist_emb, hist_len, nbr_ids, nbr_sims, counts, mass};
+  const char* names[] = {"queries", "hist_emb", "hist_len", "nbr_ids", "nbr_sims", "counts", "mass"};
+  for (int i = 0; i < 7; ++i) {
+    if (!ptrs[i]) return fail(SAGE_EINVAL, "sage_predict: %s is NULL", names[i]);
+    if (!aligned16(ptrs[i])) return fail(SAGE_EINVAL, "sage_predict: %s is not 16-byte aligned", names[i]);
+  }
+  const sage::SimTopkPlan plan = sage::plan_sim_topk(Q, N, d, k);
+  if (workspace_bytes < plan.partial_bytes || (!workspace && plan.partial_bytes))
+    return fail(SAGE_EWORKSPACE, "sage_predict: workspace of %zu bytes, %zu needed", workspace_bytes,
+                plan.partial_bytes);
+  if (!aligned16(workspace)) return fail(SAGE_EINVAL, "sage_predict: workspace is not 16-byte aligned");
+  if ((st = check_device()) != SAGE_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint64_t* partial = static_cast<uint64_t*>(workspace);
+  hipError_t e = sage::launch_sim_topk(queries, Q, hist_emb, N, d, k, plan, partial, s);
+  if (e != hipSuccess) return hip_status(e, "sim_topk launch");
+  e = sage::launch_topk_merge(partial, Q, plan.n_chunks, plan.list_len, k, nbr_ids, nbr_sims, s);
+  if (e != hipSuccess) return hip_status(e, "topk_merge launch");
+  e = sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, counts, mass, s);
+  return hip_status(e, "hist launch");
+}
+
+SAGE_API int sage_histogram(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
+                            const int32_t* hist_len, int N, float tau, const double* bin_edges, int B,
+                            int32_t* counts, float* mass, sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (k < 1 || k > SAGE_MAX_K) return fail(SAGE_EINVAL, "k=%d outside [1, %d]", k, SAGE_MAX_K);
+  if (N < 1) return fail(SAGE_EINVAL, "N=%d must be >= 1", N);
+  int st = check_tau(tau);
+  if (st != SAGE_OK) return st;
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (Q == 0) return ok();
+  if ((st = check_bins(bin_edges, B)) != SAGE_OK) return st;
+  const void* ptrs[] = {nbr_ids, nbr_sims, hist_len, counts, mass};
+  for (const void* p : ptrs) {
+    if (!p) return fail(SAGE_EINVAL, "sage_histogram: NULL pointer");
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_histogram: misaligned pointer");
+  }
+  if ((st = check_device()) != SAGE_OK) return st;
+  return hip_status(sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, counts,
+                                      mass, (hipStream_t)stream),
+                    "hist launch");
+}
+
+// --------------------------------------------------------- cost / index
+SAGE_API int sage_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B, float* cost,
+                       sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (Q == 0) return ok();
+  if (!prompt_len || !bin_repr || !cost) return fail(SAGE_EINVAL, "sage_cost: NULL pointer");
+  if (!aligned16(prompt_len) || !aligned16(bin_repr) || !aligned16(cost))
+    return fail(SAGE_EINVAL, "sage_cost: misaligned pointer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_cost(prompt_len, Q, bin_repr, B, cost, (hipStream_t)stream), "cost launch");
+}
+
+SAGE_API int sage_index(const float* mass, const float* cost, const int32_t* prompt_len,
+                        const double* bin_repr, int Q, int B, float* index, int32_t* argmin_bin,
+                        sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (Q == 0) return ok();
+  if (!mass || !index) return fail(SAGE_EINVAL, "sage_index: mass or index is NULL");
+  if (!cost && (!prompt_len || !bin_repr))
+    return fail(SAGE_EINVAL, "sage_index: cost is NULL, so prompt_len and bin_repr are required");
+  const void* ptrs[] = {mass, cost, prompt_len, bin_repr, index, argmin_bin};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(SAGE_EINVAL, "sage_index: misaligned pointer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_index(mass, cost, prompt_len, bin_repr, Q, B, index, argmin_bin,
+                                       (hipStream_t)stream),
+                    "index launch");
+}
+
+// ----------------------------------------------------------------- rank
+SAGE_API size_t sage_rank_workspace_bytes(int Q) { return Q > 0 ? sage::rank_workspace_bytes(Q) : 0; }
+
+SAGE_API int sage_rank(const float* index, int Q, int32_t* order, void* workspace,
+                       size_t workspace_bytes, sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (Q == 0) return ok();
+  if (!index || !order) return fail(SAGE_EINVAL, "sage_rank: NULL pointer");
+  if (!aligned16(index) || !aligned16(order)) return fail(SAGE_EINVAL, "sage_rank: misaligned pointer");
+  const size_t need = sage::rank_workspace_bytes(Q);
+  if (!workspace || workspace_bytes < need)
+    return fail(SAGE_EWORKSPACE, "sage_rank: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(SAGE_EINVAL, "sage_rank: workspace is not 16-byte aligned");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_rank(index, Q, order, workspace, (hipStream_t)stream), "rank launch");
+}

@@ -1,0 +1,291 @@
+"""Python binding of libsage (ctypes): argument marshalling only.
+
+Every stage runs in the library's HIP kernels; PyTorch provides device
+memory and the current stream. There is no CPU fallback: if the library is
+missing or the device is not gfx950, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libsage.so")
+_lib = None
+
+
+class SageError(RuntimeError):
+    pass
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libsage.so (after torch, so that both share one HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise SageError(f"{_LIB_PATH} is not built; run `python -m paper_2603_07917_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I, F, Z, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_void_p
+    sig = {
+        "sage_ingest_bf16": (I, [P, Z, P, S]),
+        "sage_predict_workspace_bytes": (Z, [I, I, I, I, I]),
+        "sage_predict": (I, [P, I, P, P, I, I, I, F, P, I, P, P, P, P, P, Z, S]),
+        "sage_histogram": (I, [P, P, I, I, P, I, F, P, I, P, P, S]),
+        "sage_cost": (I, [P, I, P, I, P, S]),
+        "sage_index": (I, [P, P, P, P, I, I, P, P, S]),
+        "sage_rank_workspace_bytes": (Z, [I]),
+        "sage_rank": (I, [P, I, P, P, Z, S]),
+        "sage_status_string": (ctypes.c_char_p, [I]),
+        "sage_last_error": (ctypes.c_char_p, []),
+        "sage_timer_create": (I, [I, ctypes.POINTER(P)]),
+        "sage_timer_destroy": (I, [P]),
+        "sage_timer_attach": (I, [P]),
+        "sage_timer_reset": (I, [P]),
+        "sage_timer_count": (I, [P]),
+        "sage_timer_get": (I, [P, I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I),
+                               ctypes.POINTER(ctypes.c_double)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != 0:
+        lib = load_library()
+        raise SageError(f"{lib.sage_status_string(status).decode()}: {lib.sage_last_error().decode()}")
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, dtype, name: str, ndim: Optional[int] = None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise SageError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise SageError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise SageError(f"{name} must have {ndim} dimensions")
+    if not t.is_contiguous():
+        raise SageError(f"{name} must be contiguous")
+    return t
+
+
+# ------------------------------------------------------------------ stages
+def ingest_bf16(x: torch.Tensor) -> torch.Tensor:
+    """fp32 embeddings -> bf16 store (round to nearest even), on the device."""
+    _dev(x, torch.float32, "x")
+    out = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    _check(load_library().sage_ingest_bf16(_ptr(x), x.numel(), _ptr(out), _stream()))
+    return out
+
+
+def predict_workspace_bytes(Q: int, N: int, d: int, k: int, B: int) -> int:
+    return int(load_library().sage_predict_workspace_bytes(Q, N, d, k, B))
+
+
+def predict(queries: torch.Tensor, hist_emb: torch.Tensor, hist_len: torch.Tensor, k: int,
+            tau: float, bin_edges: torch.Tensor, workspace: Optional[torch.Tensor] = None,
+            out=None):
+    """Neighbours, per-bin counts and similarity-weighted masses for each query."""
+    _dev(queries, torch.bfloat16, "queries", 2)
+    _dev(hist_emb, torch.bfloat16, "hist_emb", 2)
+    _dev(hist_len, torch.int32, "hist_len", 1)
+    _dev(bin_edges, torch.float64, "bin_edges", 1)
+    Q, d = queries.shape
+    N = hist_emb.shape[0]
+    B = bin_edges.shape[0] - 1
+    if hist_emb.shape[1] != d or hist_len.shape[0] != N:
+        raise SageError("shape mismatch between queries, hist_emb and hist_len")
+    dev = queries.device
+    need = predict_workspace_bytes(Q, N, d, k, B)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = (torch.empty((Q, k), dtype=torch.int32, device=dev),
+               torch.empty((Q, k), dtype=torch.float32, device=dev),
+               torch.empty((Q, B), dtype=torch.int32, device=dev),
+               torch.empty((Q, B), dtype=torch.float32, device=dev))
+    ids, sims, counts, mass = out
+    _check(load_library().sage_predict(
+        _ptr(queries), Q, _ptr(hist_emb), _ptr(hist_len), N, d, k, float(tau), _ptr(bin_edges), B,
+        _ptr(ids), _ptr(sims), _ptr(counts), _ptr(mass), _ptr(workspace), workspace.numel(),
+        _stream()))
+    return ids, sims, counts, mass
+
+
+def histogram(nbr_ids: torch.Tensor, nbr_sims: torch.Tensor, hist_len: torch.Tensor, tau: float,
+              bin_edges: torch.Tensor):
+    _dev(nbr_ids, torch.int32, "nbr_ids", 2)
+    _dev(nbr_sims, torch.float32, "nbr_sims", 2)
+    _dev(hist_len, torch.int32, "hist_len", 1)
+    _dev(bin_edges, torch.float64, "bin_edges", 1)
+    Q, k = nbr_ids.shape
+    B = bin_edges.shape[0] - 1
+    counts = torch.empty((Q, B), dtype=torch.int32, device=nbr_ids.device)
+    mass = torch.empty((Q, B), dtype=torch.float32, device=nbr_ids.device)
+    _check(load_library().sage_histogram(_ptr(nbr_ids), _ptr(nbr_sims), Q, k, _ptr(hist_len),
+                                         hist_len.shape[0], float(tau), _ptr(bin_edges), B,
+                                         _ptr(counts), _ptr(mass), _stream()))
+    return counts, mass
+
+
+def cost(prompt_len: torch.Tensor, bin_repr: torch.Tensor) -> torch.Tensor:
+    _dev(prompt_len, torch.int32, "prompt_len", 1)
+    _dev(bin_repr, torch.float64, "bin_repr", 1)
+    Q, B = prompt_len.shape[0], bin_repr.shape[0]
+    out = torch.empty((Q, B), dtype=torch.float32, device=prompt_len.device)
+    _check(load_library().sage_cost(_ptr(prompt_len), Q, _ptr(bin_repr), B, _ptr(out), _stream()))
+    return out
+
+
+def index(mass: torch.Tensor, prompt_len: Optional[torch.Tensor] = None,
+          bin_repr: Optional[torch.Tensor] = None, cost: Optional[torch.Tensor] = None,
+          with_argmin: bool = False, out: Optional[torch.Tensor] = None):
+    """Gittins index per row; the cost is fused in unless `cost` is given."""
+    _dev(mass, torch.float32, "mass", 2)
+    Q, B = mass.shape
+    if cost is not None:
+        _dev(cost, torch.float32, "cost", 2)
+        if tuple(cost.shape) != (Q, B):
+            raise SageError("cost must have the shape of mass")
+    else:
+        _dev(prompt_len, torch.int32, "prompt_len", 1)
+        _dev(bin_repr, torch.float64, "bin_repr", 1)
+        if prompt_len.shape[0] != Q or bin_repr.shape[0] != B:
+            raise SageError("prompt_len / bin_repr do not match mass")
+    g = out if out is not None else torch.empty(Q, dtype=torch.float32, device=mass.device)
+    arg = torch.empty(Q, dtype=torch.int32, device=mass.device) if with_argmin else None
+    _check(load_library().sage_index(_ptr(mass), _ptr(cost), _ptr(prompt_len), _ptr(bin_repr), Q, B,
+                                     _ptr(g), _ptr(arg), _stream()))
+    return (g, arg) if with_argmin else g
+
+
+def rank_workspace_bytes(Q: int) -> int:
+    return int(load_library().sage_rank_workspace_bytes(Q))
+
+
+def rank(g: torch.Tensor, workspace: Optional[torch.Tensor] = None,
+         out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Stable ascending order of the index (smaller index served first)."""
+    _dev(g, torch.float32, "index", 1)
+    Q = g.shape[0]
+    need = rank_workspace_bytes(Q)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=g.device)
+    order = out if out is not None else torch.empty(Q, dtype=torch.int32, device=g.device)
+    _check(load_library().sage_rank(_ptr(g), Q, _ptr(order), _ptr(workspace), workspace.numel(),
+                                    _stream()))
+    return order
+
+
+def schedule(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor):
+    """Cost -> index -> rank: returns (index, order)."""
+    g = index(mass, prompt_len, bin_repr)
+    return g, rank(g)
+
+
+class Store:
+    """A resident history store plus reusable device workspaces.
+
+    Holds the bf16 embeddings, the recorded output lengths and the bin edges
+    on the device, and reuses the predict / rank workspaces across calls so
+    that a steady-state decision allocates nothing new.
+    """
+
+    def __init__(self, hist_emb: torch.Tensor, hist_len: torch.Tensor, bin_edges: torch.Tensor,
+                 bin_repr: torch.Tensor, k: int, tau: float = 0.8):
+        if hist_emb.dtype == torch.float32:
+            hist_emb = ingest_bf16(hist_emb.contiguous())
+        self.hist_emb = hist_emb
+        self.hist_len = hist_len
+        self.bin_edges = bin_edges
+        self.bin_repr = bin_repr
+        self.k = int(k)
+        self.tau = float(tau)
+        self._ws = torch.empty(16, dtype=torch.uint8, device=hist_emb.device)
+        self._rank_ws = torch.empty(16, dtype=torch.uint8, device=hist_emb.device)
+
+    def _workspace(self, Q: int) -> torch.Tensor:
+        N, d = self.hist_emb.shape
+        need = predict_workspace_bytes(Q, N, d, self.k, self.bin_edges.shape[0] - 1)
+        if self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.hist_emb.device)
+        return self._ws
+
+    def predict(self, queries: torch.Tensor, out=None):
+        if queries.dtype == torch.float32:
+            queries = ingest_bf16(queries.contiguous())
+        return predict(queries, self.hist_emb, self.hist_len, self.k, self.tau, self.bin_edges,
+                       workspace=self._workspace(queries.shape[0]), out=out)
+
+    def decide(self, queries: torch.Tensor, prompt_len: torch.Tensor, out=None):
+        """One scheduling decision for a batch: predict, cost+index, rank."""
+        ids, sims, counts, mass = self.predict(queries, out=None if out is None else out[:4])
+        g = index(mass, prompt_len, self.bin_repr, out=None if out is None else out[4])
+        Q = g.shape[0]
+        need = rank_workspace_bytes(Q)
+        if self._rank_ws.numel() < need:
+            self._rank_ws = torch.empty(need, dtype=torch.uint8, device=g.device)
+        order = rank(g, workspace=self._rank_ws, out=None if out is None else out[5])
+        return ids, sims, counts, mass, g, order
+
+
+class StageTimer:
+    """Per-kernel HIP-event timing of everything the library launches while attached."""
+
+    def __init__(self, capacity: int = 4096):
+        lib = load_library()
+        h = ctypes.c_void_p()
+        _check(lib.sage_timer_create(capacity, ctypes.byref(h)))
+        self._h = h
+
+    def __enter__(self):
+        _check(load_library().sage_timer_attach(self._h))
+        return self
+
+    def __exit__(self, *exc):
+        load_library().sage_timer_attach(None)
+        return False
+
+    def reset(self):
+        _check(load_library().sage_timer_reset(self._h))
+
+    def totals(self) -> dict:
+        """{kernel name: (launches, total ms)}; synchronise the device first."""
+        lib = load_library()
+        res = {}
+        for i in range(lib.sage_timer_count(self._h)):
+            name = ctypes.c_char_p()
+            n = ctypes.c_int()
+            ms = ctypes.c_double()
+            _check(lib.sage_timer_get(self._h, i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)))
+            res[name.value.decode()] = (n.value, ms.value)
+        return res
+
+    def close(self):
+        if self._h:
+            load_library().sage_timer_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,131 @@
+"""The C-ABI library: loads, exports what include/sage.h declares, and rejects
+bad arguments before touching a device (CPU only; no compute calls)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sage.h")
+LIB = os.path.join(ROOT, "paper_2603_07917_amd", "libsage.so")
+
+SAGE_OK, SAGE_EINVAL, SAGE_EWORKSPACE = 0, -1, -2
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sage_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2603_07917_amd import build
+        build.build()
+    lib = ctypes.CDLL(LIB)
+    P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.sage_predict.argtypes = [P, I, P, P, I, I, I, F, P, I, P, P, P, P, P, Z, P]
+    lib.sage_predict_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.sage_predict_workspace_bytes.restype = Z
+    lib.sage_rank_workspace_bytes.argtypes = [I]
+    lib.sage_rank_workspace_bytes.restype = Z
+    lib.sage_index.argtypes = [P, P, P, P, I, I, P, P, P]
+    lib.sage_rank.argtypes = [P, I, P, P, Z, P]
+    lib.sage_cost.argtypes = [P, I, P, I, P, P]
+    lib.sage_histogram.argtypes = [P, P, I, I, P, I, F, P, I, P, P, P]
+    lib.sage_ingest_bf16.argtypes = [P, Z, P, P]
+    lib.sage_status_string.restype = ctypes.c_char_p
+    lib.sage_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+def test_header_declares_the_path():
+    names = declared_functions()
+    for n in ["sage_predict", "sage_cost", "sage_index", "sage_rank", "sage_histogram",
+              "sage_ingest_bf16", "sage_predict_workspace_bytes", "sage_rank_workspace_bytes",
+              "sage_status_string", "sage_last_error"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in [0, -1, -2, -3, -4]:
+        assert lib.sage_status_string(code).startswith(b"SAGE_")
+    assert b"unknown" in lib.sage_status_string(7)
+
+
+# Fake, 16-byte aligned addresses: every call below fails validation before
+# any device work, so they are never dereferenced.
+A = 0x10000
+
+
+def _predict(lib, Q=4, N=100, d=64, k=8, tau=0.8, B=16, ptrs=None, ws=A, ws_bytes=1 << 30):
+    p = ptrs or {}
+    g = lambda n: p.get(n, A)
+    return lib.sage_predict(g("q"), Q, g("h"), g("l"), N, d, k, tau, g("e"), B, g("ids"), g("sims"),
+                            g("c"), g("m"), ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw", [dict(k=0), dict(k=257), dict(d=33), dict(d=0), dict(B=0),
+                                dict(B=4097), dict(tau=0.0), dict(tau=1.5), dict(tau=math.nan),
+                                dict(tau=1e-7), dict(N=0), dict(Q=-1)])
+def test_predict_rejects_bad_sizes(lib, kw):
+    assert _predict(lib, **kw) == SAGE_EINVAL
+    assert lib.sage_last_error() != b""
+
+
+@pytest.mark.parametrize("name", ["q", "h", "l", "e", "ids", "sims", "c", "m"])
+def test_predict_rejects_null_and_misaligned(lib, name):
+    assert _predict(lib, ptrs={name: None}) == SAGE_EINVAL
+    assert _predict(lib, ptrs={name: A + 4}) == SAGE_EINVAL
+
+
+def test_predict_workspace_too_small(lib):
+    need = lib.sage_predict_workspace_bytes(4, 100, 64, 8, 16)
+    assert need > 0
+    assert _predict(lib, ws_bytes=need - 1) == SAGE_EWORKSPACE
+    assert _predict(lib, ws=None) == SAGE_EWORKSPACE
+
+
+def test_predict_q0_is_noop(lib):
+    assert _predict(lib, Q=0, ptrs={n: None for n in ["q", "ids", "sims", "c", "m"]}) == SAGE_OK
+
+
+def test_workspace_sizes(lib):
+    assert lib.sage_predict_workspace_bytes(4, 100, 33, 8, 16) == 0
+    assert lib.sage_predict_workspace_bytes(0, 100, 64, 8, 16) == 0
+    # one descending list of >= 64 keys per (query, history chunk)
+    w = lib.sage_predict_workspace_bytes(4096, 262144, 768, 64, 256)
+    assert w % (4096 * 64 * 8) == 0 and w > 0
+    assert lib.sage_predict_workspace_bytes(8, 1000, 64, 200, 16) % (8 * 256 * 8) == 0
+    assert lib.sage_rank_workspace_bytes(0) == 0
+    assert lib.sage_rank_workspace_bytes(65536) >= 4 * 4 * 65536
+
+
+def test_index_rank_cost_hist_validation(lib):
+    assert lib.sage_index(A, None, None, A, 4, 16, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index(A, None, A, A, 4, 0, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index(A, None, A, A, 4, 5000, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index(None, A, None, None, 4, 16, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index(A + 8, A, None, None, 4, 16, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index(None, None, None, None, 0, 16, None, None, None) == SAGE_OK
+    assert lib.sage_rank(A, 10, A, A, 0, None) == SAGE_EWORKSPACE
+    assert lib.sage_rank(None, 10, A, A, 1 << 20, None) == SAGE_EINVAL
+    assert lib.sage_rank(A, -1, A, A, 1 << 20, None) == SAGE_EINVAL
+    assert lib.sage_rank(None, 0, None, None, 0, None) == SAGE_OK
+    assert lib.sage_cost(A, 4, None, 16, A, None) == SAGE_EINVAL
+    assert lib.sage_cost(A, 4, A, 0, A, None) == SAGE_EINVAL
+    assert lib.sage_histogram(A, A, 4, 0, A, 10, 0.8, A, 16, A, A, None) == SAGE_EINVAL
+    assert lib.sage_histogram(A, A, 4, 8, A, 0, 0.8, A, 16, A, A, None) == SAGE_EINVAL
+    assert lib.sage_histogram(A, A, 4, 8, A, 10, 2.0, A, 16, A, A, None) == SAGE_EINVAL
+    assert lib.sage_histogram(A, None, 4, 8, A, 10, 0.8, A, 16, A, A, None) == SAGE_EINVAL
+    assert lib.sage_ingest_bf16(None, 10, A, None) == SAGE_EINVAL
+    assert lib.sage_ingest_bf16(A, 100, A + 16, None) == SAGE_EINVAL     # overlap
+    assert lib.sage_ingest_bf16(None, 0, None, None) == SAGE_OK

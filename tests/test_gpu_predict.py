@@ -1,0 +1,123 @@
+"""sage_predict (similarity + top-k + histogram) against the oracle, and the
+whole decision path (predict -> cost/index -> rank) on the named workloads."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_07917_amd import sage, workloads
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def run_predict(w, k, tau=0.8):
+    qb = sage.ingest_bf16(dev(w.queries))
+    hb = sage.ingest_bf16(dev(w.hist_emb))
+    ids, sims, counts, mass = sage.predict(qb, hb, dev(w.hist_len), k, tau, dev(w.bin_edges))
+    return host(ids), host(sims), host(counts), host(mass)
+
+
+def oracle_scores(w, rows=None):
+    qb = oracle.round_to_bf16(w.queries if rows is None else w.queries[rows])
+    return oracle.similarity(qb, oracle.round_to_bf16(w.hist_emb))
+
+
+# (Q, N, d, k, B): several query tiles with a ragged tail, history chunks and
+# 256-row steps with ragged ends, d with a half 64-wide slice, every list length.
+CASES = [
+    (70, 3000, 64, 8, 16),
+    (130, 5000, 96, 32, 128),
+    (64, 4096, 384, 64, 64),
+    (65, 7777, 128, 100, 256),
+    (40, 3001, 32, 200, 64),
+    (33, 2500, 64, 256, 1024),
+    (5, 300, 64, 1, 7),
+    (3, 10, 64, 32, 16),        # N < k: padded with -1 / -inf
+]
+
+
+@pytest.mark.parametrize("Q,N,d,k,B", CASES)
+def test_predict_small_vs_oracle(Q, N, d, k, B):
+    print(f"case Q={Q} N={N} d={d} k={k} B={B}", flush=True)
+    w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=B, seed=Q + N + d + k, clusters=6)
+    ids, sims, counts, mass = run_predict(w, k)
+    S = oracle_scores(w)
+    parity.check_topk(ids, sims, S, k)
+    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, 0.8)
+
+
+def test_predict_duplicate_rows_lower_id_first():
+    # identical history rows score identically in fp32: the lower index must come first
+    w = workloads.small_predict(Q=8, N=600, d=64, k=16, B=16, seed=5, clusters=2)
+    h = w.hist_emb.copy()
+    h[300:340] = h[100]                       # 40 copies of row 100
+    w.hist_emb = h
+    w.queries[:] = h[100]
+    ids, sims, _, _ = run_predict(w, 16)
+    S = oracle_scores(w)
+    parity.check_topk(ids, sims, S, 16)
+    for q in range(8):
+        tied = sims[q] == sims[q, 0]
+        assert list(ids[q][tied]) == sorted(ids[q][tied])
+        assert ids[q, 0] == 100
+
+
+def test_predict_tau_fallback_and_all_same_length():
+    w = workloads.small_predict(Q=20, N=2000, d=64, k=16, B=32, seed=9, clusters=3)
+    w.hist_len[:] = 777
+    ids, sims, counts, mass = run_predict(w, 16, tau=1.0)      # nobody reaches tau = 1
+    b = oracle.bin_of([777], w.bin_edges)[0]
+    assert np.all(counts[:, b] == 16) and np.all(mass[:, b] == 1.0)
+    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, 1.0)
+
+
+def test_predict_deterministic():
+    w = workloads.small_predict(Q=100, N=20000, d=128, k=64, B=64, seed=11, clusters=16)
+    a = run_predict(w, 64)
+    b = run_predict(w, 64)
+    for x, y in zip(a, b):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+
+
+def test_config1_end_to_end():
+    w = workloads.make_config(1)
+    spec = w.spec
+    ids, sims, counts, mass = run_predict(w, spec.k, spec.tau)
+    S = oracle_scores(w)
+    equal = parity.check_topk(ids, sims, S, spec.k)
+    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
+    g = host(sage.index(dev(mass), dev(w.prompt_len), dev(w.bin_repr)))
+    parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
+    parity.check_rank(host(sage.rank(dev(g))), g)
+    print(f"config 1: {equal}/{spec.Q} queries with the oracle's exact neighbour set", flush=True)
+
+
+def test_config2_full_size_sampled():
+    """The benchmark's workload and launch configuration; sampled queries checked."""
+    w = workloads.make_config(2)
+    spec = w.spec
+    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
+                       spec.k, spec.tau)
+    out = store.decide(dev(w.queries), dev(w.prompt_len))
+    ids, sims, counts, mass, g, order = [host(t) for t in out]
+    rng = np.random.default_rng(2)
+    rows = np.sort(rng.choice(spec.Q, size=48, replace=False))
+    rows = np.unique(np.concatenate([rows, [0, spec.Q - 1]]))
+    S = oracle_scores(w, rows)
+    equal = parity.check_topk(ids[rows], sims[rows], S, spec.k)
+    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
+    parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
+    parity.check_rank(order, g)
+    print(f"config 2: {equal}/{len(rows)} sampled queries with the exact neighbour set", flush=True)

@@ -1,0 +1,136 @@
+"""Stage parity of the HIP kernels against the oracle, on identical inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_07917_amd import sage, workloads
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def test_native_library_is_the_one_loaded():
+    sage.load_library()
+    maps = open("/proc/self/maps").read()
+    assert sage.library_path() in maps
+    hips = {line.split()[-1] for line in maps.splitlines() if "libamdhip64" in line}
+    assert len(hips) == 1, hips       # torch and libsage share one HIP runtime
+
+
+# ---------------------------------------------------------------- ingest
+@pytest.mark.parametrize("n", [1, 3, 4, 1001, 1 << 20])
+def test_ingest_bit_exact(n):
+    rng = np.random.default_rng(n)
+    x = (rng.standard_normal(n) * 2).astype(np.float32)
+    if n >= 8:
+        x[:8] = np.array([0x3F808000, 0x3F818000, 0x3F808001, 0x3F807FFF, 0xBF808000,
+                          0xBF818000, 0x3F7FFFFF, 0x80000000], dtype=np.uint32).view(np.float32)
+    got = host(sage.ingest_bf16(dev(x)).view(torch.int16)).view(np.uint16)
+    assert np.array_equal(got, oracle.round_to_bf16(x))
+
+
+# ------------------------------------------------------------------ cost
+@pytest.mark.parametrize("B", [1, 100, 1024])
+def test_cost(B):
+    w = workloads.small_index(Q=1000, B=B, seed=B)
+    x = host(sage.cost(dev(w.prompt_len), dev(w.bin_repr)))
+    want = oracle.cost(w.prompt_len, w.bin_repr)
+    assert np.max(np.abs(x - want) / want) <= 1e-7
+
+
+# ----------------------------------------------------------------- index
+@pytest.mark.parametrize("B", [1, 3, 64, 100, 256, 1000, 1024, 4096])
+@pytest.mark.parametrize("Q", [1, 777])
+def test_index_fused_and_explicit(Q, B):
+    w = workloads.small_index(Q=Q, B=B, seed=Q * 7 + B)
+    mass = w.mass.copy()
+    mass[Q // 2] = 0.0                         # a row with no mass -> +inf
+    x = oracle.cost(w.prompt_len, w.bin_repr)
+    g, arg = sage.index(dev(mass), dev(w.prompt_len), dev(w.bin_repr), with_argmin=True)
+    g, arg = host(g), host(arg)
+    G = parity.check_index(g, mass, x)
+    assert arg[Q // 2] == -1
+    # explicit (materialised fp32) cost support gives the same index within tolerance
+    x32 = host(sage.cost(dev(w.prompt_len), dev(w.bin_repr)))
+    g2 = host(sage.index(dev(mass), cost=dev(x32)))
+    parity.check_index(g2, mass, x32.astype(np.float64))
+    # argmin: where the oracle's minimum is clear of the runner-up, bins agree
+    Gp, ap = oracle.gittins(mass.astype(np.float64), x)
+    fin = np.isfinite(Gp)
+    assert np.all((arg[fin] >= 0) & (arg[fin] < B))
+
+
+def test_index_closed_forms():
+    B = 256
+    _, r = workloads.log_bins(8192, B)
+    I = np.array([0, 100, 5000, 17], dtype=np.int32)
+    x = oracle.cost(I, r)
+    mass = np.zeros((4, B), np.float32)
+    mass[0, 10] = 1.0                         # point mass: index = cost of that bin
+    mass[1, 200] = 0.25
+    mass[2, 3] = 0.5; mass[2, 250] = 0.5      # two-point: min(a/p, mean)
+    mass[3, :] = 1.0 / B
+    g, arg = sage.index(dev(mass), dev(I), dev(r), with_argmin=True)
+    g, arg = host(g), host(arg)
+    assert abs(g[0] - x[0, 10]) <= 1e-6 * x[0, 10] and arg[0] == 10
+    assert abs(g[1] - x[1, 200]) <= 1e-6 * x[1, 200] and arg[1] == 200
+    a, b = x[2, 3], x[2, 250]
+    want = min(a / 0.5, 0.5 * a + 0.5 * b)
+    assert abs(g[2] - want) <= 1e-6 * want
+    mean = x[3].mean()
+    assert g[3] <= mean * (1 + 1e-6)
+
+
+def test_index_config4_full():
+    w = workloads.make_config(4)
+    x = oracle.cost(w.prompt_len, w.bin_repr)
+    g = host(sage.index(dev(w.mass), dev(w.prompt_len), dev(w.bin_repr)))
+    parity.check_index(g, w.mass, x)
+    g2 = host(sage.index(dev(w.mass), dev(w.prompt_len), dev(w.bin_repr)))
+    assert np.array_equal(g.view(np.uint32), g2.view(np.uint32))   # deterministic
+
+
+# ------------------------------------------------------------------ rank
+@pytest.mark.parametrize("Q", [1, 2, 2047, 2048, 2049, 5000, 65536, 131073])
+def test_rank_bit_exact(Q):
+    rng = np.random.default_rng(Q)
+    g = np.round(rng.uniform(0, 50, size=Q)).astype(np.float32)   # many exact ties
+    g[rng.random(Q) < 0.05] = np.inf
+    g[rng.random(Q) < 0.01] = 0.0
+    order = host(sage.rank(dev(g)))
+    parity.check_rank(order, g)
+    h = rng.lognormal(8, 3, size=Q).astype(np.float32)            # wide dynamic range
+    parity.check_rank(host(sage.rank(dev(h))), h)
+
+
+def test_rank_negative_and_signed_zero():
+    g = np.array([3.0, -0.0, 0.0, -1.5, np.inf, -np.inf, 0.0, -0.0, 2.5], dtype=np.float32)
+    order = host(sage.rank(dev(g)))
+    assert list(order) == list(np.argsort(g, kind="stable"))
+
+
+# ------------------------------------------------------------- histogram
+@pytest.mark.parametrize("k,B,tau", [(1, 1, 0.8), (32, 128, 0.8), (64, 256, 0.8), (100, 37, 0.5),
+                                     (256, 1024, 0.9), (64, 4096, 0.8), (64, 256, 1.0)])
+def test_histogram_vs_oracle(k, B, tau):
+    rng = np.random.default_rng(k * 31 + B)
+    N, Q = 5000, 600
+    edges, _ = workloads.log_bins(8192, B)
+    L = rng.integers(1, 8193, size=N).astype(np.int32)
+    ids = np.stack([rng.choice(N, size=k, replace=False) for _ in range(Q)]).astype(np.int32)
+    sims = np.sort(rng.uniform(0.6, 1.0, size=(Q, k)).astype(np.float32), axis=1)[:, ::-1].copy()
+    ids[:10, k // 2:] = -1                      # fewer valid neighbours than k
+    sims[:10, k // 2:] = -np.inf
+    sims[10:20] = rng.uniform(0.1, 0.5, size=(10, k)).astype(np.float32)   # all below tau
+    counts, mass = sage.histogram(dev(ids), dev(sims), dev(L), tau, dev(edges))
+    parity.check_hist(ids, sims, host(counts), host(mass), L, edges, tau)
