@@ -1,0 +1,199 @@
+"""Benchmark of the scheduling-decision path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+A step is one scheduling decision for a batch of pending requests: bf16
+ingest of the query embeddings, similarity search + top-k + histogram
+(sage_predict), fused cost + Gittins index (sage_index) and the queue
+ranking (sage_rank). Inputs (the history store, the queries, the prompt
+lengths) are resident in HBM before the timed region starts. Prints one JSON
+line with the whole-job throughput in decisions per second, the roofline of
+the dominant kernel (HIP events over the timed region) and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="run one plain device copy of this many MiB first (counter calibration)")
+    return ap.parse_args()
+
+
+def read_traffic(kernel: str, workload_key: str):
+    """HBM bytes per launch from the committed counter summary, if still current."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_key}_traffic.txt")
+    src = os.path.join(ROOT, "paper_2603_07917_amd", "csrc", "k_sim_topk.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if kv.get("kernel_source_sha256_16") != sha:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, budget_s: float):
+    """The oracle (as it stands) on a bounded sample of the same batch."""
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    spec = w.spec
+    hb = oracle.round_to_bf16(w.hist_emb)          # the resident store: not timed, as on the GPU
+    block = 128
+    done = 0
+    t_total = 0.0
+    while done < spec.Q and t_total < budget_s:
+        rows = slice(done, min(spec.Q, done + block))
+        t0 = time.perf_counter()
+        qb = oracle.round_to_bf16(w.queries[rows])
+        ids, sims = oracle.search(qb, hb, spec.k, block=block, threads=threads)
+        counts, mass = oracle.histogram(ids, sims, w.hist_len, w.bin_edges, spec.tau)
+        G, arg, order = oracle.schedule(mass, w.prompt_len[rows], w.bin_repr)
+        t_total += time.perf_counter() - t0
+        done = rows.stop
+    return {"value": done / t_total, "unit": "decisions/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {done} of the {spec.Q} requests of one batch (full history), "
+                      f"{t_total:.1f} s of CPU time; ranking within the sample"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    from paper_2603_07917_amd import sage, workloads
+
+    torch.cuda.set_device(0)
+    w = workloads.make_config(args.config)
+    spec = w.spec
+    Q, N, d, k, B = spec.Q, spec.N, spec.d, spec.k, spec.B
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    # Resident inputs (untimed): history store ingested to bf16 once.
+    hist_f32 = dev(w.hist_emb)
+    hist = sage.ingest_bf16(hist_f32)
+    del hist_f32
+    hist_len = dev(w.hist_len)
+    edges = dev(w.bin_edges)
+    repr_ = dev(w.bin_repr)
+    queries_f32 = dev(w.queries)
+    prompt_len = dev(w.prompt_len)
+
+    # Preallocated outputs and workspaces: a step allocates nothing.
+    qb = torch.empty((Q, d), dtype=torch.bfloat16, device="cuda")
+    ids = torch.empty((Q, k), dtype=torch.int32, device="cuda")
+    sims = torch.empty((Q, k), dtype=torch.float32, device="cuda")
+    counts = torch.empty((Q, B), dtype=torch.int32, device="cuda")
+    mass = torch.empty((Q, B), dtype=torch.float32, device="cuda")
+    g = torch.empty(Q, dtype=torch.float32, device="cuda")
+    order = torch.empty(Q, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(16, sage.predict_workspace_bytes(Q, N, d, k, B)), dtype=torch.uint8, device="cuda")
+    rws = torch.empty(max(16, sage.rank_workspace_bytes(Q)), dtype=torch.uint8, device="cuda")
+    lib = sage.load_library()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        sage._check(lib.sage_ingest_bf16(queries_f32.data_ptr(), Q * d, qb.data_ptr(), stream))
+        sage._check(lib.sage_predict(qb.data_ptr(), Q, hist.data_ptr(), hist_len.data_ptr(), N, d, k,
+                                     float(spec.tau), edges.data_ptr(), B, ids.data_ptr(),
+                                     sims.data_ptr(), counts.data_ptr(), mass.data_ptr(),
+                                     ws.data_ptr(), ws.numel(), stream))
+        sage._check(lib.sage_index(mass.data_ptr(), None, prompt_len.data_ptr(), repr_.data_ptr(), Q,
+                                   B, g.data_ptr(), None, stream))
+        sage._check(lib.sage_rank(g.data_ptr(), Q, order.data_ptr(), rws.data_ptr(), rws.numel(),
+                                  stream))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    timer = sage.StageTimer(capacity=64 * (args.steps + 1))
+    with timer:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    stages = timer.totals()
+    timer.close()
+    print(f"# step: {1e3 * elapsed / args.steps:.3f} ms", file=sys.stderr, flush=True)
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = Q * args.steps / elapsed
+    n_launch, k1_ms = stages["sim_topk"]
+    k1_avg_s = k1_ms / n_launch / 1e3
+    flops = 2.0 * Q * N * d
+    achieved = flops / k1_avg_s / 1e12
+    workload_key = f"config{args.config}"
+    traffic = read_traffic("sim_topk", workload_key)
+
+    line = {
+        "metric": "scheduling decisions/sec (predict+cost+index+rank)",
+        "value": value,
+        "unit": "decisions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": workloads.WORKLOAD_NAMES[args.config], "Q": Q, "N": N, "d": d,
+                   "k": k, "B": B, "tau": spec.tau, "seed": w.seed},
+        "roofline": {"bound": "mfma", "kernel": "sim_topk", "achieved": achieved,
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
+                     "avg_launch_us": k1_avg_s * 1e6, "flops_per_launch": flops},
+        "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

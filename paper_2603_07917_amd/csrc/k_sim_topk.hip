@@ -2,31 +2,30 @@
 // Sec. 3.1: brute-force cosine similarity of prompt embeddings against the
 // history store; unit vectors make it an inner product).
 //
-// One workgroup (4 wavefronts) owns a tile of BQ queries and a contiguous
-// chunk of history rows, and walks the chunk in steps of 256 rows:
+// GEMM core (shared by the two kernels below). A workgroup of 4 wavefronts
+// multiplies one step of 256 history rows by a tile of BQ queries:
+// S^T[256 x BQ] = H_step[256 x d] * Q_tile^T with v_mfma_f32_32x32x16_bf16
+// (fp32 accumulate). Wave w owns history rows [64w, 64w + 64) of the step and
+// all BQ queries. The d axis is walked in 64-wide slices (128-byte row
+// pieces) staged through LDS (rows padded to 144 bytes, which keeps the
+// 16-byte MFMA operand reads free of bank conflicts); the next slice is
+// fetched into registers while the current one is multiplied. The scores of
+// a step depend only on (step, query tile), so both kernels compute
+// bit-identical scores for the same (query, row) pair.
 //
-//  * MFMA: S^T[256 x BQ] = H_step[256 x d] * Q_tile^T with
-//    v_mfma_f32_32x32x16_bf16 (fp32 accumulate). Both operands are staged
-//    through LDS in 64-wide d slices; the next slice is fetched into
-//    registers while the current one is multiplied. Wave w computes history
-//    rows [64w, 64w + 64) of the step against all BQ queries. Scores stay in
-//    registers; nothing of S reaches HBM.
-//  * Filter: a lane owns (query, 16 rows) pieces of the accumulator tile and
-//    compares each score with the query's threshold theta (the k-th best key
-//    of the query's list so far; -inf until k keys exist). History indices
-//    grow along the walk, so a later row with the same score loses the tie:
-//    a strict ">" is exact.
-//  * Append: survivors are packed as 64-bit keys (score bits made monotone,
-//    then ~index) and appended to a per-query buffer of 64 keys in LDS at a
-//    deterministic position (prefix over lanes). When a step brings more
-//    survivors than the buffer holds, the append runs in rounds of 64 with a
-//    merge between rounds.
-//  * Merge: the wave owning a query sorts the buffer (bitonic, across lanes)
-//    and folds it into the query's descending list of KL keys with one
-//    bitonic merge; theta becomes the list's k-th key.
-//
-// At the end of the chunk every list is written to the partial buffer
-// [Q][chunks][KL]; a second kernel merges a query's lists across chunks.
+// threshold_sample_kernel: for every query, the maxima of disjoint 16-row
+//   groups over a sample of steps (every SR-th step). The k-th largest
+//   group maximum is a score reached by k distinct history rows, hence a
+//   valid lower bound theta0 on the query's k-th best score.
+// sim_topk_kernel: one workgroup owns a query tile and a chunk of history
+//   rows. After each step, a lane compares its scores with the query's
+//   thresholds (>= theta0, and > the k-th key of the chunk list so far: rows
+//   come in index order, so a later equal score loses the tie), appends the
+//   survivors as 64-bit keys (monotone score bits, then ~index) to a per-query
+//   LDS buffer at deterministic positions (in rounds of 64 with merges in
+//   between when a step brings more), and the wave owning the query folds
+//   full buffers into the query's descending list with a bitonic merge. The
+//   lists end in the partial buffer [Q][chunks][KL].
 #include "sage_device.hpp"
 #include "sage_internal.hpp"
 
@@ -39,28 +38,116 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 constexpr int kThreads = 256;
 constexpr int kStepRows = 256;     // history rows per step (64 per wave)
 constexpr int kKT = 64;            // d elements per LDS slice
-constexpr int kLdsRow = kKT + 8;   // padded LDS row (bf16 elements): 144 bytes
-constexpr int kCap = 64;           // per-query candidate buffer
+constexpr int kRowE = kKT + 8;     // padded LDS row: 72 bf16 = 144 bytes
+constexpr int kCap = 64;           // per-query candidate buffer (keys)
 
-template <int NQT, int KL>
-struct Smem {
+template <int NQT>
+struct Core {
   static constexpr int BQ = 32 * NQT;
-  uint64_t list[BQ * KL];
-  uint64_t buf[BQ * kCap];
-  uint16_t a_tile[kStepRows * kLdsRow];
-  uint16_t b_tile[BQ * kLdsRow];
-  float theta[BQ];
-  int fill[BQ];
-  int tot[BQ];
-  int cnt[BQ * 8];
-  int rounds;
+  static constexpr int A_LD = kStepRows * kKT / 8 / kThreads;    // 16-byte loads / thread
+  static constexpr int B_CHUNKS = BQ * kKT / 8;
+  static constexpr int B_LD = (B_CHUNKS + kThreads - 1) / kThreads;
+  uint4 ra[A_LD];
+  uint4 rb[B_LD];
+
+  // Loads are unconditional (rows clamped into range) so that no branch sits
+  // around them; only the zero-fill of columns past d is a select. Rows past
+  // h_end and queries past Q carry real but unused data (masked later).
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ hist, int h0, int h_last,
+                                       const uint16_t* __restrict__ queries, int q0, int q_last,
+                                       int d, int kt) {
+    const int tid = threadIdx.x;
+    const int k0 = kt * kKT;
+#pragma unroll
+    for (int c = 0; c < A_LD; ++c) {
+      const int f = c * kThreads + tid;
+      const int row = f >> 3, col = k0 + (f & 7) * 8;
+      const int h = min(h0 + row, h_last);
+      const uint4 v = *reinterpret_cast<const uint4*>(hist + (size_t)h * d + min(col, d - 8));
+      ra[c] = col < d ? v : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int c = 0; c < B_LD; ++c) {
+      const int f = min(c * kThreads + tid, B_CHUNKS - 1);
+      const int row = f >> 3, col = k0 + (f & 7) * 8;
+      const int q = min(q0 + row, q_last);
+      const uint4 v = *reinterpret_cast<const uint4*>(queries + (size_t)q * d + min(col, d - 8));
+      rb[c] = col < d ? v : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ __forceinline__ void store(uint16_t* a_tile, uint16_t* b_tile) const {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int c = 0; c < A_LD; ++c) {
+      const int f = c * kThreads + tid;
+      *reinterpret_cast<uint4*>(a_tile + (f >> 3) * kRowE + (f & 7) * 8) = ra[c];
+    }
+#pragma unroll
+    for (int c = 0; c < B_LD; ++c) {
+      const int f = c * kThreads + tid;
+      if (B_CHUNKS % kThreads == 0 || f < B_CHUNKS)
+        *reinterpret_cast<uint4*>(b_tile + (f >> 3) * kRowE + (f & 7) * 8) = rb[c];
+    }
+  }
 };
+
+template <int NQT>
+__device__ __forceinline__ void mfma_slice(floatx16 (&acc)[2][NQT], const uint16_t* a_tile,
+                                           const uint16_t* b_tile, int w, int l32, int half) {
+  const uint16_t* as = a_tile + (64 * w + l32) * kRowE + half * 8;
+  const uint16_t* bs = b_tile + l32 * kRowE + half * 8;
+#pragma unroll
+  for (int kk = 0; kk < kKT / 16; ++kk) {
+    bf16x8 af[2], bfr[NQT];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) af[u] = *reinterpret_cast<const bf16x8*>(as + 32 * u * kRowE + kk * 16);
+#pragma unroll
+    for (int t = 0; t < NQT; ++t) bfr[t] = *reinterpret_cast<const bf16x8*>(bs + 32 * t * kRowE + kk * 16);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int t = 0; t < NQT; ++t)
+        acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[u], bfr[t], acc[u][t], 0, 0, 0);
+  }
+}
+
+// Scores of one step: acc[u][t][v] = S[h][q] with
+//   h = h0 + 64w + 32u + 8(v/4) + 4*half + (v%4),  q = q0 + 32t + l32.
+template <int NQT>
+__device__ __forceinline__ void gemm_step(floatx16 (&acc)[2][NQT], const uint16_t* __restrict__ hist,
+                                          int h0, int h_end, const uint16_t* __restrict__ queries,
+                                          int q0, int Q, int d, uint16_t* a_tile, uint16_t* b_tile) {
+  const int lane = (int)lane_id();
+  const int w = threadIdx.x / kWave;
+  const int l32 = lane & 31, half = lane >> 5;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int t = 0; t < NQT; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[u][t][v] = 0.0f;
+  const int nk = (d + kKT - 1) / kKT;
+  const int h_last = h_end - 1, q_last = Q - 1;
+  Core<NQT> core;
+  core.load(hist, h0, h_last, queries, q0, q_last, d, 0);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    __syncthreads();
+    core.store(a_tile, b_tile);
+    __syncthreads();
+    core.load(hist, h0, h_last, queries, q0, q_last, d, kt + 1);
+    mfma_slice<NQT>(acc, a_tile, b_tile, w, l32, half);
+  }
+  __syncthreads();
+  core.store(a_tile, b_tile);
+  __syncthreads();
+  mfma_slice<NQT>(acc, a_tile, b_tile, w, l32, half);
+}
 
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 __device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a > b ? b : a; }
 
-// Fold `n_buf` unsorted keys of `buf` into the descending list of KL keys and
-// return the key at position k-1 (broadcast to every lane).
+// Fold `n_buf` (<= 64) unsorted keys of `buf` into the descending list of KL
+// keys and return the list key at position k-1 (the same value in every lane).
 template <int KL>
 __device__ uint64_t merge_into_list(uint64_t* list, const uint64_t* buf, int n_buf, int k) {
   constexpr int S = KL / 64;
@@ -96,120 +183,136 @@ __device__ uint64_t merge_into_list(uint64_t* list, const uint64_t* buf, int n_b
   return shfl_u64(sel, kl);
 }
 
+// ------------------------------------------------------------------------
+// Sampled group maxima: one workgroup per (query tile, sampled step).
+// gm[q][s][g] for the 16 groups of 16 rows of a step; -inf past N.
+// ------------------------------------------------------------------------
+template <int NQT>
+__global__ void __launch_bounds__(kThreads, 1) threshold_sample_kernel(
+    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    int sample_every, int n_samples, float* __restrict__ gm) {
+  constexpr int BQ = 32 * NQT;
+  __shared__ __align__(16) uint16_t a_tile[kStepRows * kRowE];
+  __shared__ __align__(16) uint16_t b_tile[BQ * kRowE];
+  const int q0 = blockIdx.x * BQ;
+  const int s = blockIdx.y;
+  const int h0 = s * sample_every * kStepRows;
+  const int h_end = min(N, h0 + kStepRows);
+  floatx16 acc[2][NQT];
+  gemm_step<NQT>(acc, hist, h0, h_end, queries, q0, Q, d, a_tile, b_tile);
+
+  const int lane = (int)lane_id();
+  const int w = threadIdx.x / kWave;
+  const int l32 = lane & 31, half = lane >> 5;
+#pragma unroll
+  for (int t = 0; t < NQT; ++t) {
+    const int q = q0 + 32 * t + l32;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      float m = -__builtin_inff();
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int h = h0 + 64 * w + 32 * u + 8 * (v >> 2) + 4 * half + (v & 3);
+        if (h < h_end) m = fmaxf(m, acc[u][t][v]);
+      }
+      if (q < Q) gm[((size_t)q * n_samples + s) * 16 + w * 4 + half * 2 + u] = m;
+    }
+  }
+}
+
+// theta0[q] = k-th largest of the query's m group maxima (-inf when fewer
+// than k exist): bitonic sort in LDS, one workgroup per query.
+__global__ void __launch_bounds__(256) threshold_select_kernel(const float* __restrict__ gm, int m,
+                                                               int m_pow2, int k,
+                                                               float* __restrict__ theta0) {
+  extern __shared__ float vals[];
+  const int q = blockIdx.x;
+  const float* src = gm + (size_t)q * m;
+  for (int i = threadIdx.x; i < m_pow2; i += 256) vals[i] = i < m ? src[i] : -__builtin_inff();
+  __syncthreads();
+  for (int size = 2; size <= m_pow2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int e = threadIdx.x; e < m_pow2 / 2; e += 256) {
+        const int i = (e / stride) * (2 * stride) + (e % stride);
+        const int j = i + stride;
+        const bool desc = (i & size) == 0;
+        const float a = vals[i], b = vals[j];
+        if ((a < b) == desc) { vals[i] = b; vals[j] = a; }
+      }
+      __syncthreads();
+    }
+  }
+  if (threadIdx.x == 0) theta0[q] = k <= m ? vals[k - 1] : -__builtin_inff();
+}
+
+// ------------------------------------------------------------------------
+// Main kernel.
+// ------------------------------------------------------------------------
+template <int NQT, int KL>
+struct TopkSmem {
+  static constexpr int BQ = 32 * NQT;
+  uint64_t list[BQ * KL];
+  uint64_t buf[BQ * kCap];
+  uint16_t a_tile[kStepRows * kRowE];
+  uint16_t b_tile[BQ * kRowE];
+  float theta[BQ];
+  float theta0[BQ];
+  int fill[BQ];
+  int tot[BQ];
+  int cnt[BQ * 8];
+  int rounds;
+};
+
 template <int NQT, int KL>
 __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
-    int k, int chunk_rows, int n_chunks, uint64_t* __restrict__ partial) {
+    int k, int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0,
+    uint64_t* __restrict__ partial) {
   constexpr int BQ = 32 * NQT;
-  constexpr int QPW = BQ / 4;                // queries owned (merged) by each wave
-  constexpr int A_CHUNKS = kStepRows * kKT / 8 / kThreads;   // 16-byte loads per thread
-  constexpr int B_CHUNKS = (BQ * kKT / 8 + kThreads - 1) / kThreads;
-  __shared__ Smem<NQT, KL> sm;
+  constexpr int QPW = BQ / 4;              // queries merged by each wave
+  __shared__ __align__(16) TopkSmem<NQT, KL> sm;
 
+  // Block -> (query tile, chunk). When the chunks split evenly over the 8
+  // XCDs, the query tiles of one chunk are dispatched to the same XCD so that
+  // its history rows are shared through that XCD's L2.
+  int qt, chunk;
+  const int b = blockIdx.x;
+  if (n_chunks % 8 == 0) {
+    const int x = b & 7, slot = b >> 3;
+    chunk = x + 8 * (slot / q_tiles);
+    qt = slot % q_tiles;
+  } else {
+    chunk = b / q_tiles;
+    qt = b % q_tiles;
+  }
   const int tid = threadIdx.x;
   const int lane = (int)lane_id();
   const int w = tid / kWave;
-  const int half = lane >> 5;
-  const int l32 = lane & 31;
-  const int q0 = blockIdx.x * BQ;
-  const int chunk = blockIdx.y;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int q0 = qt * BQ;
   const int h_begin = chunk * chunk_rows;
   const int h_end = min(N, h_begin + chunk_rows);
 
   for (int i = tid; i < BQ * KL; i += kThreads) sm.list[i] = kPadKey;
   for (int i = tid; i < BQ; i += kThreads) {
     sm.theta[i] = -__builtin_inff();
+    sm.theta0[i] = (theta0 && q0 + i < Q) ? theta0[q0 + i] : -__builtin_inff();
     sm.fill[i] = 0;
   }
 
-  const int n_kt = (d + kKT - 1) / kKT;
-  uint4 ra[A_CHUNKS];
-  uint4 rb[B_CHUNKS];
-
   for (int h0 = h_begin; h0 < h_end; h0 += kStepRows) {
     floatx16 acc[2][NQT];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int t = 0; t < NQT; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[u][t][v] = 0.0f;
+    const int step_end = min(h_end, h0 + kStepRows);
+    gemm_step<NQT>(acc, hist, h0, step_end, queries, q0, Q, d, sm.a_tile, sm.b_tile);
 
-    auto load_slice = [&](int kt) {
-      const int k0 = kt * kKT;
-#pragma unroll
-      for (int c = 0; c < A_CHUNKS; ++c) {
-        const int flat = c * kThreads + tid;
-        const int row = flat >> 3, col = (flat & 7) * 8;
-        const int h = h0 + row;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (h < h_end && k0 + col < d)
-          v = *reinterpret_cast<const uint4*>(hist + (size_t)h * d + k0 + col);
-        ra[c] = v;
-      }
-#pragma unroll
-      for (int c = 0; c < B_CHUNKS; ++c) {
-        const int flat = c * kThreads + tid;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (flat < BQ * kKT / 8) {
-          const int row = flat >> 3, col = (flat & 7) * 8;
-          const int q = q0 + row;
-          if (q < Q && k0 + col < d)
-            v = *reinterpret_cast<const uint4*>(queries + (size_t)q * d + k0 + col);
-        }
-        rb[c] = v;
-      }
-    };
-    auto store_slice = [&]() {
-#pragma unroll
-      for (int c = 0; c < A_CHUNKS; ++c) {
-        const int flat = c * kThreads + tid;
-        const int row = flat >> 3, col = (flat & 7) * 8;
-        *reinterpret_cast<uint4*>(&sm.a_tile[row * kLdsRow + col]) = ra[c];
-      }
-#pragma unroll
-      for (int c = 0; c < B_CHUNKS; ++c) {
-        const int flat = c * kThreads + tid;
-        if (flat < BQ * kKT / 8) {
-          const int row = flat >> 3, col = (flat & 7) * 8;
-          *reinterpret_cast<uint4*>(&sm.b_tile[row * kLdsRow + col]) = rb[c];
-        }
-      }
-    };
-
-    load_slice(0);
-    for (int kt = 0; kt < n_kt; ++kt) {
-      __syncthreads();
-      store_slice();
-      __syncthreads();
-      if (kt + 1 < n_kt) load_slice(kt + 1);
-#pragma unroll
-      for (int kk = 0; kk < kKT / 16; ++kk) {
-        const int kofs = kk * 16 + half * 8;
-        bf16x8 af[2], bfr[NQT];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-          af[u] = *reinterpret_cast<const bf16x8*>(&sm.a_tile[(64 * w + 32 * u + l32) * kLdsRow + kofs]);
-#pragma unroll
-        for (int t = 0; t < NQT; ++t)
-          bfr[t] = *reinterpret_cast<const bf16x8*>(&sm.b_tile[(32 * t + l32) * kLdsRow + kofs]);
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int t = 0; t < NQT; ++t)
-            acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[u], bfr[t], acc[u][t], 0, 0, 0);
-      }
-    }
-
-    // ---------------- epilogue: filter, rank, append, merge ----------------
-    // acc[u][t][v] holds S[h][q] with q = 32t + l32 and
-    // h = h0 + 64w + 32u + 8(v/4) + 4*half + (v%4).
-    float th[NQT];
+    // ---------------- filter, rank, append, merge ----------------
+    float th[NQT], th0[NQT];
     int my_cnt[NQT];
 #pragma unroll
     for (int t = 0; t < NQT; ++t) {
       const int ql = 32 * t + l32;
       th[t] = sm.theta[ql];
+      th0[t] = sm.theta0[ql];
       int c = 0;
       if (q0 + ql < Q) {
 #pragma unroll
@@ -217,7 +320,8 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int h = h0 + 64 * w + 32 * u + 8 * (v >> 2) + 4 * half + (v & 3);
-            c += (h < h_end && acc[u][t][v] > th[t]) ? 1 : 0;
+            const float s = acc[u][t][v];
+            c += (h < step_end && s >= th0[t] && s > th[t]) ? 1 : 0;
           }
       }
       my_cnt[t] = c;
@@ -239,9 +343,9 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
 #pragma unroll
     for (int t = 0; t < NQT; ++t) {
       const int ql = 32 * t + l32;
-      int b = sm.fill[ql];
-      for (int j = 0; j < 2 * w + half; ++j) b += sm.cnt[ql * 8 + j];
-      base[t] = b;
+      int bb = sm.fill[ql];
+      for (int j = 0; j < 2 * w + half; ++j) bb += sm.cnt[ql * 8 + j];
+      base[t] = bb;
     }
     for (int r = 0; r < rounds; ++r) {
       const int lo = r * kCap, hi = lo + kCap;
@@ -256,7 +360,7 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
           for (int v = 0; v < 16; ++v) {
             const int h = h0 + 64 * w + 32 * u + 8 * (v >> 2) + 4 * half + (v & 3);
             const float s = acc[u][t][v];
-            if (h < h_end && s > th[t]) {
+            if (h < step_end && s >= th0[t] && s > th[t]) {
               if (g >= lo && g < hi) sm.buf[ql * kCap + (g - lo)] = make_key(s, (uint32_t)h);
               ++g;
             }
@@ -297,10 +401,28 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
 
 template <int NQT, int KL>
 hipError_t launch_t(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
-                    const SimTopkPlan& plan, uint64_t* partial, hipStream_t stream) {
-  dim3 grid(plan.q_tiles, plan.n_chunks);
-  hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), grid, dim3(kThreads), 0, stream, queries, Q, hist,
-                     N, d, k, plan.chunk_rows, plan.n_chunks, partial);
+                    const SimTopkPlan& plan, uint64_t* partial, float* gm, float* theta0,
+                    hipStream_t stream) {
+  if (plan.n_samples > 0) {
+    {
+      LaunchScope scope("threshold_sample", stream);
+      hipLaunchKernelGGL((threshold_sample_kernel<NQT>), dim3(plan.q_tiles, plan.n_samples),
+                         dim3(kThreads), 0, stream, queries, Q, hist, N, d, plan.sample_every,
+                         plan.n_samples, gm);
+    }
+    const int m = plan.n_samples * 16;
+    int m2 = 1;
+    while (m2 < m) m2 <<= 1;
+    {
+      LaunchScope scope("threshold_select", stream);
+      hipLaunchKernelGGL(threshold_select_kernel, dim3(Q), dim3(256), m2 * sizeof(float), stream, gm,
+                         m, m2, k, theta0);
+    }
+  }
+  LaunchScope scope("sim_topk", stream);
+  hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), dim3(plan.q_tiles * plan.n_chunks), dim3(kThreads), 0,
+                     stream, queries, Q, hist, N, d, k, plan.chunk_rows, plan.n_chunks, plan.q_tiles,
+                     plan.n_samples > 0 ? theta0 : nullptr, partial);
   return hipGetLastError();
 }
 
@@ -314,26 +436,43 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   p.list_len = L;
   p.q_tile = L <= 128 ? 64 : 32;
   p.q_tiles = (Q + p.q_tile - 1) / p.q_tile;
-  const long max_chunks = ((long)N + kStepRows - 1) / kStepRows;
+  const long steps = ((long)N + kStepRows - 1) / kStepRows;
   long want = (1024 + (long)p.q_tiles - 1) / (long)(p.q_tiles > 0 ? p.q_tiles : 1);
+  if (want >= 8) want = (want + 7) / 8 * 8;            // whole chunks per XCD
   if (want < 1) want = 1;
-  if (want > max_chunks) want = max_chunks;
+  if (want > steps) want = steps;
   long rows = ((long)N + want - 1) / want;
   rows = (rows + kStepRows - 1) / kStepRows * kStepRows;
   p.chunk_rows = (int)rows;
   p.n_chunks = (int)(((long)N + rows - 1) / rows);
+  // Sample every SR-th step: at least 4k group maxima, at most 8192, SR <= 32.
+  p.sample_every = 0;
+  p.n_samples = 0;
+  if (steps * 16 >= 8L * k) {
+    long sr = steps * 16 / (4L * k);
+    if (sr > 32) sr = 32;
+    if (sr < 1) sr = 1;
+    while ((steps + sr - 1) / sr > 512) ++sr;
+    p.sample_every = (int)sr;
+    p.n_samples = (int)((steps + sr - 1) / sr);
+  }
   p.partial_bytes = (size_t)Q * (size_t)p.n_chunks * (size_t)L * sizeof(uint64_t);
+  p.gm_bytes = (size_t)Q * (size_t)p.n_samples * 16 * sizeof(float);
+  p.theta_bytes = (size_t)Q * sizeof(float);
   return p;
 }
 
 hipError_t launch_sim_topk(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d,
-                           int k, const SimTopkPlan& plan, uint64_t* partial, hipStream_t stream) {
+                           int k, const SimTopkPlan& plan, void* workspace, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
-  LaunchScope scope("sim_topk", stream);
+  char* ws = static_cast<char*>(workspace);
+  uint64_t* partial = reinterpret_cast<uint64_t*>(ws);
+  float* gm = reinterpret_cast<float*>(ws + plan.partial_bytes);
+  float* theta0 = reinterpret_cast<float*>(ws + plan.partial_bytes + plan.gm_bytes);
   switch (plan.list_len) {
-    case 64: return launch_t<2, 64>(queries, Q, hist, N, d, k, plan, partial, stream);
-    case 128: return launch_t<2, 128>(queries, Q, hist, N, d, k, plan, partial, stream);
-    default: return launch_t<1, 256>(queries, Q, hist, N, d, k, plan, partial, stream);
+    case 64: return launch_t<2, 64>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
+    case 128: return launch_t<2, 128>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
+    default: return launch_t<1, 256>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
   }
 }
 

@@ -228,7 +228,7 @@ SAGE_API size_t sage_predict_workspace_bytes(int Q, int N, int d, int k, int B) 
   if (check_predict_sizes(Q, N, d, k, B) != SAGE_OK) return 0;
   g_last_error = keep;
   if (Q == 0) return 0;
-  return sage::plan_sim_topk(Q, N, d, k).partial_bytes;
+  return sage::plan_sim_topk(Q, N, d, k).workspace_bytes();
 }
 
 SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_emb,
@@ -248,14 +248,14 @@ SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_e
     if (!aligned16(ptrs[i])) return fail(SAGE_EINVAL, "sage_predict: %s is not 16-byte aligned", names[i]);
   }
   const sage::SimTopkPlan plan = sage::plan_sim_topk(Q, N, d, k);
-  if (workspace_bytes < plan.partial_bytes || (!workspace && plan.partial_bytes))
+  if (workspace_bytes < plan.workspace_bytes() || !workspace)
     return fail(SAGE_EWORKSPACE, "sage_predict: workspace of %zu bytes, %zu needed", workspace_bytes,
-                plan.partial_bytes);
+                plan.workspace_bytes());
   if (!aligned16(workspace)) return fail(SAGE_EINVAL, "sage_predict: workspace is not 16-byte aligned");
   if ((st = check_device()) != SAGE_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint64_t* partial = static_cast<uint64_t*>(workspace);
-  hipError_t e = sage::launch_sim_topk(queries, Q, hist_emb, N, d, k, plan, partial, s);
+  hipError_t e = sage::launch_sim_topk(queries, Q, hist_emb, N, d, k, plan, workspace, s);
   if (e != hipSuccess) return hip_status(e, "sim_topk launch");
   e = sage::launch_topk_merge(partial, Q, plan.n_chunks, plan.list_len, k, nbr_ids, nbr_sims, s);
   if (e != hipSuccess) return hip_status(e, "topk_merge launch");

@@ -26,7 +26,12 @@ struct SimTopkPlan {
   int chunk_rows;   // history rows per workgroup (multiple of the step size)
   int n_chunks;     // workgroups along the history axis (= streams per query)
   int q_tiles;      // workgroups along the query axis
-  size_t partial_bytes;
+  int sample_every; // threshold pre-pass: every sample_every-th 256-row step
+  int n_samples;    // sampled steps (0: no pre-pass, thresholds start at -inf)
+  size_t partial_bytes;  // workspace: per-stream lists [Q][n_chunks][list_len] keys
+  size_t gm_bytes;       //            sampled group maxima [Q][n_samples][16] f32
+  size_t theta_bytes;    //            per-query threshold [Q] f32
+  size_t workspace_bytes() const { return partial_bytes + gm_bytes + theta_bytes; }
 };
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
 
@@ -41,7 +46,7 @@ hipError_t launch_index(const float* mass, const float* cost, const int32_t* pro
 size_t rank_workspace_bytes(int Q);
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream);
 hipError_t launch_sim_topk(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d,
-                           int k, const SimTopkPlan& plan, uint64_t* partial, hipStream_t stream);
+                           int k, const SimTopkPlan& plan, void* workspace, hipStream_t stream);
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
                              int32_t* ids, float* sims, hipStream_t stream);
 hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, const int32_t* hist_len,

@@ -101,10 +101,10 @@ def test_predict_q0_is_noop(lib):
 def test_workspace_sizes(lib):
     assert lib.sage_predict_workspace_bytes(4, 100, 33, 8, 16) == 0
     assert lib.sage_predict_workspace_bytes(0, 100, 64, 8, 16) == 0
-    # one descending list of >= 64 keys per (query, history chunk)
+    # at least one descending list of >= 64 keys per (query, history chunk)
     w = lib.sage_predict_workspace_bytes(4096, 262144, 768, 64, 256)
-    assert w % (4096 * 64 * 8) == 0 and w > 0
-    assert lib.sage_predict_workspace_bytes(8, 1000, 64, 200, 16) % (8 * 256 * 8) == 0
+    assert w >= 4096 * 64 * 8
+    assert lib.sage_predict_workspace_bytes(8, 1000, 64, 200, 16) >= 8 * 256 * 8
     assert lib.sage_rank_workspace_bytes(0) == 0
     assert lib.sage_rank_workspace_bytes(65536) >= 4 * 4 * 65536
 
