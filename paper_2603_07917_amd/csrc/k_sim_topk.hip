@@ -306,26 +306,37 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     gemm_step<NQT>(acc, hist, h0, step_end, queries, q0, Q, d, sm.a_tile, sm.b_tile);
 
     // ---------------- filter, rank, append, merge ----------------
-    float th[NQT], th0[NQT];
+    // One compare per score: s >= theta0 and s > theta  <=>  s > max(below(theta0), theta),
+    // where below(x) is the largest float under x. Rows past the chunk end
+    // (only in a chunk's last step) are masked out of the candidate bits.
+    const bool full_step = step_end == h0 + kStepRows;
+    float thr[NQT];
+    uint32_t bits[NQT];
     int my_cnt[NQT];
 #pragma unroll
     for (int t = 0; t < NQT; ++t) {
       const int ql = 32 * t + l32;
-      th[t] = sm.theta[ql];
-      th0[t] = sm.theta0[ql];
-      int c = 0;
-      if (q0 + ql < Q) {
+      thr[t] = fmaxf(float_below(sm.theta0[ql]), sm.theta[ql]);
+      uint32_t m = 0;
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) m |= (acc[u][t][v] > thr[t] ? 1u : 0u) << (16 * u + v);
+      if (!full_step) {
+        uint32_t valid = 0;
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int h = h0 + 64 * w + 32 * u + 8 * (v >> 2) + 4 * half + (v & 3);
-            const float s = acc[u][t][v];
-            c += (h < step_end && s >= th0[t] && s > th[t]) ? 1 : 0;
+            valid |= (h < step_end ? 1u : 0u) << (16 * u + v);
           }
+        m &= valid;
       }
-      my_cnt[t] = c;
-      sm.cnt[ql * 8 + 2 * w + half] = c;
+      if (q0 + ql >= Q) m = 0;
+      bits[t] = m;
+      my_cnt[t] = __popc(m);
+      sm.cnt[ql * 8 + 2 * w + half] = my_cnt[t];
     }
     if (tid == 0) sm.rounds = 1;
     __syncthreads();
@@ -354,17 +365,23 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
         const int ql = 32 * t + l32;
         if (my_cnt[t] == 0 || base[t] + my_cnt[t] <= lo || base[t] >= hi) continue;
         int g = base[t];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
+        uint32_t m = bits[t];
+        while (m) {
+          const int i = __ffs(m) - 1;
+          m &= m - 1;
+          if (g >= lo && g < hi) {
+            const int u = i >> 4, v = i & 15;
             const int h = h0 + 64 * w + 32 * u + 8 * (v >> 2) + 4 * half + (v & 3);
-            const float s = acc[u][t][v];
-            if (h < step_end && s >= th0[t] && s > th[t]) {
-              if (g >= lo && g < hi) sm.buf[ql * kCap + (g - lo)] = make_key(s, (uint32_t)h);
-              ++g;
-            }
+            float sv = 0.0f;
+#pragma unroll
+            for (int uu = 0; uu < 2; ++uu)
+#pragma unroll
+              for (int vv = 0; vv < 16; ++vv)
+                if (16 * uu + vv == i) sv = acc[uu][t][vv];
+            sm.buf[ql * kCap + (g - lo)] = make_key(sv, (uint32_t)h);
           }
+          ++g;
+        }
       }
       __syncthreads();
       if (r + 1 < rounds) {

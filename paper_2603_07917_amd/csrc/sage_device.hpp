@@ -25,6 +25,14 @@ __device__ __forceinline__ float f32_from_order_bits(uint32_t o) {
 __device__ __forceinline__ uint64_t make_key(float s, uint32_t n) {
   return ((uint64_t)f32_order_bits(s) << 32) | (uint64_t)(~n);
 }
+// Largest float below x (x finite or -inf; -inf maps to itself).
+__device__ __forceinline__ float float_below(float x) {
+  if (x == -__builtin_inff()) return x;
+  if (x == 0.0f) return -1.401298464e-45f;            // below both zeros
+  const uint32_t u = __float_as_uint(x);
+  return __uint_as_float(x > 0.0f ? u - 1u : u + 1u);
+}
+
 // Padding key: similarity -inf, index -1. Every real candidate beats it.
 constexpr uint64_t kPadKey = (uint64_t)0x007FFFFFu << 32;
 
