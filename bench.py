@@ -43,10 +43,13 @@ def parse():
 
 
 def read_traffic(kernel: str, workload_key: str):
-    """HBM bytes per launch from the committed counter summary, if still current."""
+    """HBM bytes per launch from the committed counter summary, if still current.
+
+    The summary records a hash of the kernel sources the counters were taken
+    on; after any change to them the figure is stale and None is returned.
+    """
     import hashlib
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_key}_traffic.txt")
-    src = os.path.join(ROOT, "paper_2603_07917_amd", "csrc", "k_sim_topk.hip")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -54,8 +57,10 @@ def read_traffic(kernel: str, workload_key: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if kv.get("kernel_source_sha256_16") != sha:
+    h = hashlib.sha256()
+    for src in ("k_sim_topk.hip", "sage_device.hpp"):
+        h.update(open(os.path.join(ROOT, "paper_2603_07917_amd", "csrc", src), "rb").read())
+    if kv.get("kernel_source_sha256_16") != h.hexdigest()[:16]:
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
