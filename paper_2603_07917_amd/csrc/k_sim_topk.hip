@@ -39,7 +39,8 @@ constexpr int kThreads = 256;
 constexpr int kStepRows = 256;     // history rows per step (64 per wave)
 constexpr int kKT = 64;            // d elements per LDS slice
 constexpr int kRowE = kKT + 8;     // padded LDS row: 72 bf16 = 144 bytes
-constexpr int kCap = 64;           // per-query candidate buffer (keys)
+// Per-query candidate buffer: 64 keys, or 32 for 128-query tiles (LDS budget).
+template <int NQT> struct CapOf { static constexpr int value = NQT >= 4 ? 32 : 64; };
 
 template <int NQT>
 struct Core {
@@ -251,6 +252,7 @@ __global__ void __launch_bounds__(256) threshold_select_kernel(const float* __re
 template <int NQT, int KL>
 struct TopkSmem {
   static constexpr int BQ = 32 * NQT;
+  static constexpr int kCap = CapOf<NQT>::value;
   uint64_t list[BQ * KL];
   uint64_t buf[BQ * kCap];
   uint16_t a_tile[kStepRows * kRowE];
@@ -270,6 +272,7 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     uint64_t* __restrict__ partial) {
   constexpr int BQ = 32 * NQT;
   constexpr int QPW = BQ / 4;              // queries merged by each wave
+  constexpr int kCap = CapOf<NQT>::value;
   __shared__ __align__(16) TopkSmem<NQT, KL> sm;
 
   // Block -> (query tile, chunk). When the chunks split evenly over the 8
@@ -451,7 +454,7 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   int L = 64;
   while (L < k) L <<= 1;
   p.list_len = L;
-  p.q_tile = L <= 128 ? 64 : 32;
+  p.q_tile = L == 64 ? 128 : (L == 128 ? 64 : 32);
   p.q_tiles = (Q + p.q_tile - 1) / p.q_tile;
   const long steps = ((long)N + kStepRows - 1) / kStepRows;
   long want = (1024 + (long)p.q_tiles - 1) / (long)(p.q_tiles > 0 ? p.q_tiles : 1);
@@ -487,7 +490,7 @@ hipError_t launch_sim_topk(const uint16_t* queries, int Q, const uint16_t* hist,
   float* gm = reinterpret_cast<float*>(ws + plan.partial_bytes);
   float* theta0 = reinterpret_cast<float*>(ws + plan.partial_bytes + plan.gm_bytes);
   switch (plan.list_len) {
-    case 64: return launch_t<2, 64>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
+    case 64: return launch_t<4, 64>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
     case 128: return launch_t<2, 128>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
     default: return launch_t<1, 256>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
   }
