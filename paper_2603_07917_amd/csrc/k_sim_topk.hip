@@ -269,7 +269,7 @@ template <int NQT, int KL>
 __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
     int k, int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0,
-    uint64_t* __restrict__ partial) {
+    const int* __restrict__ only_flagged, uint64_t* __restrict__ partial) {
   constexpr int BQ = 32 * NQT;
   constexpr int QPW = BQ / 4;              // queries merged by each wave
   constexpr int kCap = CapOf<NQT>::value;
@@ -295,6 +295,16 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
   const int q0 = qt * BQ;
   const int h_begin = chunk * chunk_rows;
   const int h_end = min(N, h_begin + chunk_rows);
+
+  // As the exact fallback of the filtered path, only tiles holding a flagged
+  // query do any work.
+  if (only_flagged) {
+    if (tid == 0) sm.rounds = 0;
+    __syncthreads();
+    if (tid < BQ && q0 + tid < Q && only_flagged[q0 + tid]) sm.rounds = 1;
+    __syncthreads();
+    if (sm.rounds == 0) return;
+  }
 
   for (int i = tid; i < BQ * KL; i += kThreads) sm.list[i] = kPadKey;
   for (int i = tid; i < BQ; i += kThreads) {
@@ -419,31 +429,426 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
   }
 }
 
-template <int NQT, int KL>
-hipError_t launch_t(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
-                    const SimTopkPlan& plan, uint64_t* partial, float* gm, float* theta0,
-                    hipStream_t stream) {
-  if (plan.n_samples > 0) {
-    {
-      LaunchScope scope("threshold_sample", stream);
-      hipLaunchKernelGGL((threshold_sample_kernel<NQT>), dim3(plan.q_tiles, plan.n_samples),
-                         dim3(kThreads), 0, stream, queries, Q, hist, N, d, plan.sample_every,
-                         plan.n_samples, gm);
+
+// ========================================================================
+// Filtered path for k <= 64.
+//
+// Ring core: a workgroup multiplies 256 history rows by 256 queries per
+// step; wave w = 2*wh + wq owns the 128 x 128 block of rows wh and queries
+// wq (4 x 4 MFMA 32x32x16 tiles, 256 accumulators). The d axis is walked in
+// 32-wide slices held in a ring of four LDS stages (512 rows x 64 bytes
+// each). Stages are filled by direct global->LDS loads (16 bytes per lane,
+// no registers): waves 0-1 move history rows, waves 2-3 query rows, three
+// slices ahead of the MFMAs and straight across step boundaries, so the
+// pipeline never drains between steps. One barrier per slice.
+// ========================================================================
+namespace ring {
+
+constexpr int kKT = 32;                          // bf16 columns per slice
+constexpr int kStages = 4;
+constexpr int kStageBytes = 512 * kKT * 2;       // 32 KiB
+constexpr int kBQ = 256;                         // queries per tile
+constexpr int kLoads = 8;                        // 16-byte loads per lane per slice
+constexpr int kAhead = kStages - 1;              // slices in flight
+
+// 16-byte chunk c (0..3) of LDS row r is stored at position c ^ swz(r):
+// eight lanes reading one chunk of eight consecutive rows (the MFMA operand
+// pattern) then hit eight different 16-byte bank groups.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// LDS[m0 + 16*lane] = 16 bytes at base + off (gfx950 global_load_lds_dwordx4).
+// Issued from inline assembly so that the compiler does not serialise LDS
+// reads of other stages behind it; completion is tracked with wait_loads.
+__device__ __forceinline__ void load_to_lds(const void* base, uint32_t off, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(m0) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory"); }
+// Workgroup barrier that first retires this wave's LDS reads.
+__device__ __forceinline__ void barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+struct Frags {
+  bf16x8 a[4], b[4];
+};
+
+// Keeps a tile in accumulator registers up to this point of the program, so
+// that epilogues copy tiles out one at a time (bounded register use).
+__device__ __forceinline__ void pin(floatx16& x) { asm volatile("" : "+a"(x)); }
+
+__device__ __forceinline__ void mma(floatx16 (&acc)[4][4], const Frags& f) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[u], f.b[t], acc[u][t], 0, 0, 0);
+}
+
+// Runs steps h0 = h_first + j * h_stride (j < n_steps) of query tile q0 and
+// calls epi(acc, h0, step_end) after each, step_end = min(h_limit, h0 + 256),
+// with acc[u][t][v] = S[h][q] for
+//   h = h0 + 128 wh + 32 u + 8 (v / 4) + 4 half + v % 4,  q = q0 + 128 wq + 32 t + l32.
+// Rows past N - 1 and queries past Q - 1 are read clamped (their scores are
+// meaningless and must be masked by the caller). Requires d % 32 == 0.
+template <class Epi>
+__device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, int h_first, int h_stride,
+                                      int n_steps, int h_limit, const uint16_t* __restrict__ queries, int Q,
+                                      int q0, int d, char* lds, Epi& epi) {
+  const int lane = (int)lane_id();
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int wh = w >> 1, wq = w & 1;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int nk = d / kKT;
+  const int total = n_steps * nk;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+
+  // Loader: slot (8w + i) * 64 + lane of a stage holds chunk (lane & 3) ^ swz
+  // of LDS row 16 (8w + i) + lane / 4, i.e. row r0 + 16 i (r0 = 128 (w & 1) +
+  // lane / 4) of this wave's operand: the history step for w < 2, the query
+  // tile otherwise. swz of that row depends on lane and on i only via i % 2.
+  const bool hist_side = w < 2;
+  const int r0 = 128 * (w & 1) + (lane >> 2);
+  const uint32_t cb0 = (uint32_t)(((lane & 3) ^ swz(lane >> 2)) * 16);
+  const uint32_t cb1 = (uint32_t)(((lane & 3) ^ swz(16 + (lane >> 2))) * 16);
+  const uint32_t row_bytes = (uint32_t)d * 2u;
+  int ld_step = 0, ld_kt = 0;
+  const char* src = nullptr;
+  int last = 0;
+  auto issue = [&](int g) {
+    if (ld_kt == 0) {                         // next step: new source rows
+      if (hist_side) {
+        const int base_row = h_first + ld_step * h_stride;
+        src = reinterpret_cast<const char*>(hist + (size_t)base_row * d);
+        last = N - 1 - base_row;
+      } else {
+        src = reinterpret_cast<const char*>(queries + (size_t)q0 * d);
+        last = Q - 1 - q0;
+      }
     }
-    const int m = plan.n_samples * 16;
-    int m2 = 1;
-    while (m2 < m) m2 <<= 1;
-    {
-      LaunchScope scope("threshold_select", stream);
-      hipLaunchKernelGGL(threshold_select_kernel, dim3(Q), dim3(256), m2 * sizeof(float), stream, gm,
-                         m, m2, k, theta0);
+    const uint32_t m0 = lds0 + (uint32_t)((g & (kStages - 1)) * kStageBytes + w * kLoads * 1024);
+    const uint32_t kb = (uint32_t)ld_kt * (kKT * 2);
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const uint32_t off = (uint32_t)min(r0 + 16 * i, last) * row_bytes + ((i & 1) ? cb1 : cb0) + kb;
+      load_to_lds(src, off, m0 + i * 1024);
+    }
+    if (++ld_kt == nk) { ld_kt = 0; ++ld_step; }
+  };
+
+  // Operand reads: A = history rows 128 wh + 32 u + l32, B = query rows
+  // 256 + 128 wq + 32 t + l32; k chunk 2 kk + half of the slice.
+  uint32_t a_off[2], b_off[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const uint32_t pos = (uint32_t)(((2 * kk + half) ^ swz(l32)) * 16);
+    a_off[kk] = (uint32_t)((128 * wh + l32) * 64) + pos;
+    b_off[kk] = (uint32_t)((256 + 128 * wq + l32) * 64) + pos;
+  }
+  auto read = [&](int g, int kk, Frags& f) {
+    const char* stage = lds + (g & (kStages - 1)) * kStageBytes;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f.a[u] = *reinterpret_cast<const bf16x8*>(stage + a_off[kk] + u * 2048);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) f.b[t] = *reinterpret_cast<const bf16x8*>(stage + b_off[kk] + t * 2048);
+  };
+
+  __syncthreads();                              // earlier users of the LDS are done
+  const int pre = min(kAhead, total);
+  for (int g = 0; g < pre; ++g) issue(g);
+  if (pre == 3) wait_loads<2 * kLoads>();
+  else if (pre == 2) wait_loads<kLoads>();
+  else wait_loads<0>();
+  barrier();
+  Frags f0, f1;
+  read(0, 0, f0);
+  int g = 0;
+  for (int step = 0; step < n_steps; ++step) {
+    floatx16 acc[4][4];
+    // One slice: f0 holds its first 16 columns on entry; on exit f0 holds the
+    // first 16 columns of slice g + 1.
+    auto slice = [&](bool first) {
+      read(g, 1, f1);
+      if (first) {
+        const floatx16 zero = {};
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[u], f0.b[t], zero, 0, 0, 0);
+      } else {
+        mma(acc, f0);
+      }
+      // Slice g + 1 must have landed; slices up to min(total - 1, g + 2) are issued.
+      if (g + 2 < total) wait_loads<kLoads>();
+      else wait_loads<0>();
+      barrier();                                // also: all waves are done with stage (g - 1) % 4
+      if (g + kAhead < total) issue(g + kAhead);
+      if (g + 1 < total) read(g + 1, 0, f0);
+      mma(acc, f1);
+      ++g;
+    };
+    slice(true);
+    for (int kt = 1; kt < nk; ++kt) slice(false);
+    const int h0 = h_first + step * h_stride;
+    epi(acc, h0, min(h_limit, h0 + 256));
+  }
+}
+
+}  // namespace ring
+
+// Sampled group maxima with the ring core (the same scores as the filter
+// kernel): block (tile, y) runs samples y * spb .. of the sample list,
+// sample s being step s * sample_every; every sampled step is whole.
+__global__ void __launch_bounds__(kThreads, 1) threshold_sample_ring_kernel(
+    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    int sample_every, int n_samples, int spb, float* __restrict__ gm) {
+  __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
+  const int q0 = blockIdx.x * ring::kBQ;
+  const int s0 = blockIdx.y * spb;
+  const int n_steps = min(spb, n_samples - s0);
+  const int lane = (int)lane_id();
+  const int w = threadIdx.x / kWave;
+  const int wh = w >> 1, wq = w & 1;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int stride = sample_every * kStepRows;
+  // Sampled steps are whole (256 rows inside the store): no row masking.
+  auto epi = [&](floatx16 (&acc)[4][4], int h0, int) {
+    const int s = h0 / stride;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int q = q0 + 128 * wq + 32 * t + l32;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ring::pin(acc[u][t]);
+        float m = acc[u][t][0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) m = fmaxf(m, acc[u][t][v]);
+        if (q < Q) gm[((size_t)q * n_samples + s) * 16 + wh * 8 + half * 4 + u] = m;
+      }
+    }
+  };
+  ring::sweep(hist, N, s0 * stride, stride, n_steps, N, queries, Q, q0, d, lds, epi);
+}
+
+// acc[u][t][i % 16] for a lane-varying i = 16u + v: a select tree, no
+// dynamic register indexing.
+__device__ __forceinline__ float pick_score(const floatx16 (&acc)[4][4], int t, int i) {
+  float r = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) r = (i == 16 * u + v) ? acc[u][t][v] : r;
+  return r;
+}
+
+// Filter kernel: every score >= theta0[q] is written as a key to the
+// segment [q][chunk][0..seg_cap) (position from an LDS counter); the true
+// count goes to seg_count[q][chunk] even when the segment overflows.
+__global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
+    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0, int seg_cap,
+    uint64_t* __restrict__ seg, int* __restrict__ seg_count) {
+  __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
+  __shared__ int cnt[ring::kBQ];
+  int qt, chunk;
+  const int b = blockIdx.x;
+  if (n_chunks % 8 == 0) {
+    const int x = b & 7, slot = b >> 3;
+    chunk = x + 8 * (slot / q_tiles);
+    qt = slot % q_tiles;
+  } else {
+    chunk = b / q_tiles;
+    qt = b % q_tiles;
+  }
+  const int tid = threadIdx.x;
+  const int lane = (int)lane_id();
+  const int w = tid / kWave;
+  const int wh = w >> 1, wq = w & 1;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int q0 = qt * ring::kBQ;
+  const int h_begin = chunk * chunk_rows;
+  const int h_end = min(N, h_begin + chunk_rows);
+  cnt[tid] = 0;
+  float thr[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int q = q0 + 128 * wq + 32 * t + l32;
+    thr[t] = q < Q ? float_below(theta0 ? theta0[q] : -__builtin_inff()) : __builtin_inff();
+  }
+  // Score acc[u][t][v] of this lane is row h0 + 128 wh + 4 half + r(i) for
+  // bit i = 16 u + v, r(i) = 32 (i / 16) + 8 ((i / 4) % 4) + i % 4.
+  auto epi = [&](floatx16 (&acc)[4][4], int h0, int step_end) {
+    const int lim = step_end - h0 - 128 * wh - 4 * half;     // r(i) < lim: row inside the step
+    const int hl = h0 + 128 * wh + 4 * half;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) ring::pin(acc[u][t]);
+      uint32_t lo = 0, hi = 0;
+#pragma unroll
+      for (int i = 31; i >= 0; --i) {
+        lo = 2 * lo + (acc[i >> 4][t][i & 15] > thr[t] ? 1u : 0u);
+        hi = 2 * hi + (acc[2 + (i >> 4)][t][i & 15] > thr[t] ? 1u : 0u);
+      }
+      uint64_t m = ((uint64_t)hi << 32) | lo;
+      if (step_end - h0 < kStepRows) {                          // last, partial step
+        uint64_t valid = 0;
+#pragma unroll
+        for (int i = 0; i < 64; ++i)
+          valid |= (uint64_t)(32 * (i >> 4) + 8 * ((i >> 2) & 3) + (i & 3) < lim ? 1u : 0u) << i;
+        m &= valid;
+      }
+      if (m == 0) continue;
+      const int ql = 128 * wq + 32 * t + l32;
+      const int base = atomicAdd(&cnt[ql], __popcll(m));
+      uint64_t* dst = seg + ((size_t)(q0 + ql) * n_chunks + chunk) * seg_cap;
+      for (int j = base; m && j < seg_cap; ++j) {
+        const int i = __ffsll((unsigned long long)m) - 1;
+        m &= m - 1;
+        const int h = hl + 32 * (i >> 4) + 8 * ((i >> 2) & 3) + (i & 3);
+        dst[j] = make_key(pick_score(acc, t, i), (uint32_t)h);
+      }
+    }
+  };
+  const int n_steps = (h_end - h_begin + kStepRows - 1) / kStepRows;
+  ring::sweep(hist, N, h_begin, kStepRows, n_steps, h_end, queries, Q, q0, d, lds, epi);
+  __syncthreads();
+  if (q0 + tid < Q) seg_count[(size_t)(q0 + tid) * n_chunks + chunk] = cnt[tid];
+}
+
+// Descending order of a bitonic sequence held one key per lane (half-cleaners).
+__device__ __forceinline__ uint64_t wave_bitonic_clean_desc64(uint64_t v) {
+#pragma unroll
+  for (int stride = 32; stride > 0; stride >>= 1) v = cx_lanes(v, stride, true);
+  return v;
+}
+
+// Select kernel: one workgroup (4 waves) per query. Candidate p of the
+// query's concatenated segments is found by a search of the segment offsets
+// and read straight from global memory, 64 at a time per wave. Each wave keeps
+// its best 64 keys as a descending list across lanes: a group that beats the
+// list's last key is sorted (wave bitonic sort) and folded in with
+// C_i = max(A_i, B_{63-i}) and six half-cleaner stages. Wave 0 then folds in
+// the other three lists and writes the first k. A query with an overflowed
+// segment is flagged for the exact fallback and left untouched here.
+__global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict__ seg,
+                                                     const int* __restrict__ seg_count, int n_chunks,
+                                                     int seg_cap, int k, int* __restrict__ flags,
+                                                     int32_t* __restrict__ ids, float* __restrict__ sims) {
+  __shared__ int off[kWave + 1];
+  __shared__ int over;
+  __shared__ uint64_t lists[4][kWave];
+  const int q = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = (int)lane_id();
+  const int w = tid / kWave;
+  if (w == 0) {                                       // n_chunks <= 64: one segment per lane
+    const int n = lane < n_chunks ? seg_count[(size_t)q * n_chunks + lane] : 0;
+    const int c = min(n, seg_cap);
+    int incl = c;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int y = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    off[lane] = incl - c;
+    if (lane == kWave - 1) off[kWave] = incl;
+    const bool ov = __any(n > seg_cap);
+    if (lane == 0) over = ov ? 1 : 0;
+  }
+  __syncthreads();
+  if (over) {
+    if (tid == 0) flags[q] = 1;
+    return;
+  }
+  if (tid == 0) flags[q] = 0;
+  const int total = off[kWave];
+  const uint64_t* src = seg + (size_t)q * n_chunks * seg_cap;
+  uint64_t list = kPadKey;
+  for (int base = w * kWave; base < total; base += 4 * kWave) {
+    const int p = base + lane;
+    uint64_t key = kPadKey;
+    if (p < total) {
+      int lo = 0, hi = n_chunks - 1;                  // last segment with off <= p
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= p) lo = mid;
+        else hi = mid - 1;
+      }
+      key = src[(size_t)lo * seg_cap + (p - off[lo])];
+    }
+    const uint64_t last = shfl_u64(list, kWave - 1);
+    if (!__any(key > last)) continue;
+    key = wave_sort_desc64(key);
+    const uint64_t rev = shfl_u64(key, kWave - 1 - lane);
+    list = wave_bitonic_clean_desc64(list > rev ? list : rev);
+  }
+  lists[w][lane] = list;
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int o = 1; o < 4; ++o) {
+    const uint64_t other = lists[o][kWave - 1 - lane];
+    list = wave_bitonic_clean_desc64(list > other ? list : other);
+  }
+  if (lane < k) {
+    ids[(size_t)q * k + lane] = list == kPadKey ? -1 : key_id(list);
+    sims[(size_t)q * k + lane] = list == kPadKey ? -__builtin_inff() : key_sim(list);
+  }
+}
+
+template <int NQT, int KL>
+hipError_t launch_lists(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+                        const SimTopkPlan& p, const float* theta0, const int* only_flagged,
+                        uint64_t* partial, hipStream_t stream) {
+  LaunchScope scope(only_flagged ? "sim_topk_fallback" : "sim_topk", stream);
+  hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), dim3(p.q_tiles * p.n_chunks), dim3(kThreads), 0,
+                     stream, queries, Q, hist, N, d, k, p.chunk_rows, p.n_chunks, p.q_tiles, theta0,
+                     only_flagged, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_theta(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+                        const SimTopkPlan& p, int q_tiles, bool big, float* gm, float* theta0,
+                        hipStream_t stream) {
+  {
+    LaunchScope scope("threshold_sample", stream);
+    const dim3 grid(q_tiles, p.n_samples);
+    if (big) {
+      const int spb = p.f_spb;
+      const dim3 rgrid(q_tiles, (p.n_samples + spb - 1) / spb);
+      hipLaunchKernelGGL(threshold_sample_ring_kernel, rgrid, dim3(kThreads), 0, stream, queries, Q,
+                         hist, N, d, p.sample_every, p.n_samples, spb, gm);
+    } else if (p.list_len == 128) {
+      hipLaunchKernelGGL((threshold_sample_kernel<2>), grid, dim3(kThreads), 0, stream, queries, Q,
+                         hist, N, d, p.sample_every, p.n_samples, gm);
+    } else {
+      hipLaunchKernelGGL((threshold_sample_kernel<1>), grid, dim3(kThreads), 0, stream, queries, Q,
+                         hist, N, d, p.sample_every, p.n_samples, gm);
     }
   }
-  LaunchScope scope("sim_topk", stream);
-  hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), dim3(plan.q_tiles * plan.n_chunks), dim3(kThreads), 0,
-                     stream, queries, Q, hist, N, d, k, plan.chunk_rows, plan.n_chunks, plan.q_tiles,
-                     plan.n_samples > 0 ? theta0 : nullptr, partial);
+  const int m = p.n_samples * 16;
+  int m2 = 1;
+  while (m2 < m) m2 <<= 1;
+  LaunchScope scope("threshold_select", stream);
+  hipLaunchKernelGGL(threshold_select_kernel, dim3(Q), dim3(256), m2 * sizeof(float), stream, gm, m,
+                     m2, k, theta0);
   return hipGetLastError();
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+void chunking(int q_tiles, int N, int target_blocks, int max_chunks, int* chunk_rows, int* n_chunks) {
+  const long steps = ((long)N + kStepRows - 1) / kStepRows;
+  long want = ((long)target_blocks + q_tiles - 1) / (long)(q_tiles > 0 ? q_tiles : 1);
+  if (want >= 8) want = (want + 7) / 8 * 8;            // whole chunks per XCD
+  if (want < 1) want = 1;
+  if (want > max_chunks) want = max_chunks;
+  if (want > steps) want = steps;
+  long rows = ((long)N + want - 1) / want;
+  rows = (rows + kStepRows - 1) / kStepRows * kStepRows;
+  *chunk_rows = (int)rows;
+  *n_chunks = (int)(((long)N + rows - 1) / rows);
 }
 
 }  // namespace
@@ -456,18 +861,10 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   p.list_len = L;
   p.q_tile = L == 64 ? 128 : (L == 128 ? 64 : 32);
   p.q_tiles = (Q + p.q_tile - 1) / p.q_tile;
-  const long steps = ((long)N + kStepRows - 1) / kStepRows;
-  long want = (1024 + (long)p.q_tiles - 1) / (long)(p.q_tiles > 0 ? p.q_tiles : 1);
-  if (want >= 8) want = (want + 7) / 8 * 8;            // whole chunks per XCD
-  if (want < 1) want = 1;
-  if (want > steps) want = steps;
-  long rows = ((long)N + want - 1) / want;
-  rows = (rows + kStepRows - 1) / kStepRows * kStepRows;
-  p.chunk_rows = (int)rows;
-  p.n_chunks = (int)(((long)N + rows - 1) / rows);
-  // Sample every SR-th step: at least 4k group maxima, at most 8192, SR <= 32.
-  p.sample_every = 0;
-  p.n_samples = 0;
+  chunking(p.q_tiles, N, 1024, 1 << 20, &p.chunk_rows, &p.n_chunks);
+  // Threshold pre-pass: every SR-th step, >= 4k group maxima, at most 8192, SR <= 32.
+  // Only whole steps are sampled.
+  const long steps = (long)N / kStepRows;
   if (steps * 16 >= 8L * k) {
     long sr = steps * 16 / (4L * k);
     if (sr > 32) sr = 32;
@@ -476,24 +873,73 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
     p.sample_every = (int)sr;
     p.n_samples = (int)((steps + sr - 1) / sr);
   }
-  p.partial_bytes = (size_t)Q * (size_t)p.n_chunks * (size_t)L * sizeof(uint64_t);
-  p.gm_bytes = (size_t)Q * (size_t)p.n_samples * 16 * sizeof(float);
-  p.theta_bytes = (size_t)Q * sizeof(float);
+  // Filtered path (k <= 64): 256-query tiles, segments of 8192 keys per query in all.
+  p.fast = L == 64;
+  if (p.fast) {
+    p.f_q_tiles = (Q + ring::kBQ - 1) / ring::kBQ;
+    // samples per sampling block: about one block per CU
+    p.f_spb = 1;
+    while (p.n_samples > 0 && (long)p.f_q_tiles * ((p.n_samples + 2 * p.f_spb - 1) / (2 * p.f_spb)) >= 256)
+      p.f_spb *= 2;
+    chunking(p.f_q_tiles, N, 512, 64, &p.f_chunk_rows, &p.f_n_chunks);
+    p.seg_cap = 1;                                   // power of two, n_chunks * cap <= 8192
+    while (p.seg_cap * 2 * p.f_n_chunks <= 8192) p.seg_cap *= 2;
+  }
+  size_t o = 0;
+  p.off_partial = o; o = align256(o + (size_t)Q * p.n_chunks * L * sizeof(uint64_t));
+  p.off_gm = o;      o = align256(o + (size_t)Q * p.n_samples * 16 * sizeof(float));
+  p.off_theta = o;   o = align256(o + (size_t)Q * sizeof(float));
+  if (p.fast) {
+    p.off_seg = o;    o = align256(o + (size_t)Q * p.f_n_chunks * p.seg_cap * sizeof(uint64_t));
+    p.off_segcnt = o; o = align256(o + (size_t)Q * p.f_n_chunks * sizeof(int));
+    p.off_flags = o;  o = align256(o + (size_t)Q * sizeof(int));
+  }
+  p.total_bytes = o;
   return p;
 }
 
-hipError_t launch_sim_topk(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d,
-                           int k, const SimTopkPlan& plan, void* workspace, hipStream_t stream) {
+hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+                             const SimTopkPlan& p, void* workspace, int32_t* ids, float* sims,
+                             hipStream_t stream) {
   if (Q == 0) return hipSuccess;
   char* ws = static_cast<char*>(workspace);
-  uint64_t* partial = reinterpret_cast<uint64_t*>(ws);
-  float* gm = reinterpret_cast<float*>(ws + plan.partial_bytes);
-  float* theta0 = reinterpret_cast<float*>(ws + plan.partial_bytes + plan.gm_bytes);
-  switch (plan.list_len) {
-    case 64: return launch_t<4, 64>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
-    case 128: return launch_t<2, 128>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
-    default: return launch_t<1, 256>(queries, Q, hist, N, d, k, plan, partial, gm, theta0, stream);
+  uint64_t* partial = reinterpret_cast<uint64_t*>(ws + p.off_partial);
+  float* gm = reinterpret_cast<float*>(ws + p.off_gm);
+  float* theta0 = reinterpret_cast<float*>(ws + p.off_theta);
+  hipError_t e;
+  if (p.fast) {
+    if (p.n_samples > 0) {
+      e = launch_theta(queries, Q, hist, N, d, k, p, p.f_q_tiles, true, gm, theta0, stream);
+      if (e != hipSuccess) return e;
+    }
+    uint64_t* seg = reinterpret_cast<uint64_t*>(ws + p.off_seg);
+    int* segcnt = reinterpret_cast<int*>(ws + p.off_segcnt);
+    int* flags = reinterpret_cast<int*>(ws + p.off_flags);
+    {
+      LaunchScope scope("sim_topk", stream);
+      hipLaunchKernelGGL(sim_filter_kernel, dim3(p.f_q_tiles * p.f_n_chunks), dim3(kThreads), 0, stream,
+                         queries, Q, hist, N, d, p.f_chunk_rows, p.f_n_chunks, p.f_q_tiles,
+                         p.n_samples > 0 ? theta0 : nullptr, p.seg_cap, seg, segcnt);
+    }
+    {
+      LaunchScope scope("topk_select", stream);
+      hipLaunchKernelGGL(select_kernel, dim3(Q), dim3(256), 0, stream, seg, segcnt,
+                         p.f_n_chunks, p.seg_cap, k, flags, ids, sims);
+    }
+    // Exact fallback for queries whose candidates overflowed (no work otherwise).
+    e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
+    if (e != hipSuccess) return e;
+    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, ids, sims, stream);
   }
+  if (p.n_samples > 0) {
+    e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, false, gm, theta0, stream);
+    if (e != hipSuccess) return e;
+  }
+  const float* th = p.n_samples > 0 ? theta0 : nullptr;
+  if (p.list_len == 128) e = launch_lists<2, 128>(queries, Q, hist, N, d, k, p, th, nullptr, partial, stream);
+  else e = launch_lists<1, 256>(queries, Q, hist, N, d, k, p, th, nullptr, partial, stream);
+  if (e != hipSuccess) return e;
+  return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, nullptr, ids, sims, stream);
 }
 
 }  // namespace sage

@@ -17,9 +17,10 @@ constexpr int kMergeKeys = 4096;   // LDS capacity in keys (32 KiB)
 
 __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
     const uint64_t* __restrict__ partial, int n_lists, int list_len, int k,
-    int32_t* __restrict__ ids, float* __restrict__ sims) {
+    const int* __restrict__ only_flagged, int32_t* __restrict__ ids, float* __restrict__ sims) {
   __shared__ uint64_t slot[kMergeKeys];
   const int q = blockIdx.x;
+  if (only_flagged && only_flagged[q] == 0) return;
   const int L = list_len;
   const int G = kMergeKeys / L;                 // lists per LDS batch (power of two)
   const uint64_t* src = partial + (size_t)q * n_lists * L;
@@ -71,11 +72,11 @@ __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
 }  // namespace
 
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
-                             int32_t* ids, float* sims, hipStream_t stream) {
+                             const int* only_flagged, int32_t* ids, float* sims, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
-  LaunchScope scope("topk_merge", stream);
+  LaunchScope scope(only_flagged ? "topk_merge_fallback" : "topk_merge", stream);
   hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, partial, n_lists,
-                     list_len, k, ids, sims);
+                     list_len, k, only_flagged, ids, sims);
   return hipGetLastError();
 }
 

@@ -254,11 +254,9 @@ SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_e
   if (!aligned16(workspace)) return fail(SAGE_EINVAL, "sage_predict: workspace is not 16-byte aligned");
   if ((st = check_device()) != SAGE_OK) return st;
   hipStream_t s = (hipStream_t)stream;
-  uint64_t* partial = static_cast<uint64_t*>(workspace);
-  hipError_t e = sage::launch_sim_topk(queries, Q, hist_emb, N, d, k, plan, workspace, s);
-  if (e != hipSuccess) return hip_status(e, "sim_topk launch");
-  e = sage::launch_topk_merge(partial, Q, plan.n_chunks, plan.list_len, k, nbr_ids, nbr_sims, s);
-  if (e != hipSuccess) return hip_status(e, "topk_merge launch");
+  hipError_t e = sage::launch_neighbours(queries, Q, hist_emb, N, d, k, plan, workspace, nbr_ids,
+                                         nbr_sims, s);
+  if (e != hipSuccess) return hip_status(e, "neighbour search launch");
   e = sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, counts, mass, s);
   return hip_status(e, "hist launch");
 }

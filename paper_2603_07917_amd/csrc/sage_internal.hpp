@@ -19,19 +19,25 @@ struct LaunchScope {
   hipStream_t stream_;
 };
 
-// Launch-configuration choice of the fused similarity/top-k kernel.
+// Launch plan of the neighbour search (threshold pre-pass, search, merge).
 struct SimTopkPlan {
-  int list_len;     // per-stream list length: next power of two >= k, at least 64
+  // exact per-chunk lists (the path for k > 64, and the fallback of the filtered path)
+  int list_len;     // list length: next power of two >= k, at least 64
   int q_tile;       // queries per workgroup
-  int chunk_rows;   // history rows per workgroup (multiple of the step size)
-  int n_chunks;     // workgroups along the history axis (= streams per query)
   int q_tiles;      // workgroups along the query axis
-  int sample_every; // threshold pre-pass: every sample_every-th 256-row step
-  int n_samples;    // sampled steps (0: no pre-pass, thresholds start at -inf)
-  size_t partial_bytes;  // workspace: per-stream lists [Q][n_chunks][list_len] keys
-  size_t gm_bytes;       //            sampled group maxima [Q][n_samples][16] f32
-  size_t theta_bytes;    //            per-query threshold [Q] f32
-  size_t workspace_bytes() const { return partial_bytes + gm_bytes + theta_bytes; }
+  int chunk_rows;   // history rows per workgroup (multiple of 256)
+  int n_chunks;     // workgroups along the history axis (= lists per query)
+  // threshold pre-pass: every sample_every-th 256-row step (0 samples: none)
+  int sample_every;
+  int n_samples;
+  // filtered path (k <= 64)
+  bool fast;
+  int f_q_tiles, f_chunk_rows, f_n_chunks;
+  int f_spb;        // sampled steps per threshold-sampling workgroup
+  int seg_cap;      // candidate keys per (query, chunk) segment
+  // workspace layout (byte offsets, 256-aligned)
+  size_t off_partial, off_gm, off_theta, off_seg, off_segcnt, off_flags, total_bytes;
+  size_t workspace_bytes() const { return total_bytes; }
 };
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
 
@@ -45,10 +51,13 @@ hipError_t launch_index(const float* mass, const float* cost, const int32_t* pro
                         hipStream_t stream);
 size_t rank_workspace_bytes(int Q);
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream);
-hipError_t launch_sim_topk(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d,
-                           int k, const SimTopkPlan& plan, void* workspace, hipStream_t stream);
+// Neighbours of every query: ids [Q, k] and sims [Q, k] (sorted, padded).
+hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+                             const SimTopkPlan& plan, void* workspace, int32_t* ids, float* sims,
+                             hipStream_t stream);
+// Merge of per-chunk lists; with `only_flagged`, queries whose flag is 0 are skipped.
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
-                             int32_t* ids, float* sims, hipStream_t stream);
+                             const int* only_flagged, int32_t* ids, float* sims, hipStream_t stream);
 hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, const int32_t* hist_len,
                        int N, float tau, const double* edges, int B, int32_t* counts, float* mass,
                        hipStream_t stream);

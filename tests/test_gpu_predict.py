@@ -74,6 +74,22 @@ def test_predict_duplicate_rows_lower_id_first():
         assert ids[q, 0] == 100
 
 
+def test_predict_candidate_overflow_takes_exact_fallback():
+    # Half of the store repeats one vector: queries equal to it see thousands of
+    # tied scores (far more survivors than the filtered path keeps), which must
+    # be answered exactly by the fallback; the other queries take the fast path.
+    w = workloads.small_predict(Q=12, N=12000, d=64, k=8, B=16, seed=21, clusters=4)
+    h = w.hist_emb.copy()
+    h[:6000] = h[6000]
+    w.hist_emb = h
+    w.queries[:6] = h[6000]
+    ids, sims, counts, mass = run_predict(w, 8)
+    S = oracle_scores(w)
+    parity.check_topk(ids, sims, S, 8)
+    assert list(ids[0]) == list(range(8))          # all tied: lowest indices first
+    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, 0.8)
+
+
 def test_predict_tau_fallback_and_all_same_length():
     w = workloads.small_predict(Q=20, N=2000, d=64, k=16, B=32, seed=9, clusters=3)
     w.hist_len[:] = 777
