@@ -430,6 +430,59 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
 }
 
 
+// Descending order of a bitonic sequence held one key per lane (half-cleaners).
+__device__ __forceinline__ uint64_t wave_bitonic_clean_desc64(uint64_t v) {
+#pragma unroll
+  for (int stride = 32; stride > 0; stride >>= 1) v = cx_lanes(v, stride, true);
+  return v;
+}
+
+// Folds 64 keys (one per lane, any order) into the wave's descending list of
+// its 64 largest keys: skipped when no key beats the list's last one,
+// otherwise a wave bitonic sort, C_i = max(A_i, B_{63-i}) and half-cleaners.
+__device__ __forceinline__ uint64_t fold_group(uint64_t list, uint64_t key) {
+  if (!__any(key > shfl_u64(list, kWave - 1))) return list;
+  key = wave_sort_desc64(key);
+  const uint64_t rev = shfl_u64(key, kWave - 1 - (int)lane_id());
+  return wave_bitonic_clean_desc64(list > rev ? list : rev);
+}
+
+// Wave 0 folds the lists of waves 1..3 (in LDS) into its own.
+__device__ __forceinline__ uint64_t fold_lists(uint64_t list, const uint64_t (&lists)[4][kWave]) {
+  const int lane = (int)lane_id();
+#pragma unroll
+  for (int o = 1; o < 4; ++o) {
+    const uint64_t other = lists[o][kWave - 1 - lane];
+    list = wave_bitonic_clean_desc64(list > other ? list : other);
+  }
+  return list;
+}
+
+// theta0 for k <= 64: the k-th largest of a query's m group maxima, with
+// per-wave top-64 lists in registers (keys: maximum, then position).
+__global__ void __launch_bounds__(256) threshold_select64_kernel(const float* __restrict__ gm, int m, int k,
+                                                                 float* __restrict__ theta0) {
+  __shared__ uint64_t lists[4][kWave];
+  const int q = blockIdx.x;
+  const int lane = (int)lane_id();
+  const int w = threadIdx.x / kWave;
+  const float* src = gm + (size_t)q * m;
+  uint64_t list = kPadKey;
+  int p = w * kWave + lane;
+  uint64_t next = p < m ? make_key(src[p], (uint32_t)p) : kPadKey;
+  for (int base = w * kWave; base < m; base += 4 * kWave) {
+    const uint64_t cur = next;
+    p = base + 4 * kWave + lane;
+    next = p < m ? make_key(src[p], (uint32_t)p) : kPadKey;     // prefetch
+    list = fold_group(list, cur);
+  }
+  lists[w][lane] = list;
+  __syncthreads();
+  if (w != 0) return;
+  list = fold_lists(list, lists);
+  if (lane == k - 1) theta0[q] = k <= m ? key_sim(list) : -__builtin_inff();
+}
+
 // ========================================================================
 // Filtered path for k <= 64.
 //
@@ -451,10 +504,13 @@ constexpr int kBQ = 256;                         // queries per tile
 constexpr int kLoads = 8;                        // 16-byte loads per lane per slice
 constexpr int kAhead = kStages - 1;              // slices in flight
 
-// 16-byte chunk c (0..3) of LDS row r is stored at position c ^ swz(r):
-// eight lanes reading one chunk of eight consecutive rows (the MFMA operand
-// pattern) then hit eight different 16-byte bank groups.
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// 16-byte chunk c (0..3) of LDS row r (64 bytes) is stored at position
+// c ^ swz(r). An MFMA operand read has 16 lanes reading one chunk of 16
+// consecutive rows per cycle; four rows fill the 64 four-byte banks, and
+// swz = (r / 4) % 4 gives the four rows that share banks four different
+// positions (measured: no bank conflicts, against one in three LDS cycles
+// for the unswizzled layout).
+__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
 // LDS[m0 + 16*lane] = 16 bytes at base + off (gfx950 global_load_lds_dwordx4).
 // Issued from inline assembly so that the compiler does not serialise LDS
@@ -463,10 +519,30 @@ __device__ __forceinline__ void load_to_lds(const void* base, uint32_t off, uint
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :: "v"(off), "s"(base), "s"(m0) : "memory", "m0");
 }
+// The same when the wave-uniform `enabled` is non-zero, else nothing. The
+// test is a branch inside the assembly, which keeps the surrounding MFMA
+// sequence in one basic block.
+__device__ __forceinline__ void load_to_lds_if(const void* base, uint32_t off, uint32_t m0, int enabled) {
+  asm volatile("s_cmp_eq_u32 %3, 0\n\ts_cbranch_scc1 1f\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+               "global_load_lds_dwordx4 %0, %1\n1:"
+               :: "v"(off), "s"(base), "s"(m0), "s"(enabled) : "memory", "m0", "scc");
+}
 template <int N>
 __device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory"); }
-// Workgroup barrier that first retires this wave's LDS reads.
-__device__ __forceinline__ void barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// Waits until at most n slices (n * kLoads loads) of this wave are in flight.
+__device__ __forceinline__ void wait_slices(int n) {
+  if (n <= 0) wait_loads<0>();
+  else if (n == 1) wait_loads<kLoads>();
+  else if (n == 2) wait_loads<2 * kLoads>();
+  else wait_loads<3 * kLoads>();
+}
+// Workgroup barrier that first retires this wave's LDS reads. The wait is the
+// compiler's own instruction (lgkmcnt(0), other counters untouched), so its
+// bookkeeping of outstanding LDS reads stays exact after the barrier.
+__device__ __forceinline__ void barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  asm volatile("s_barrier" ::: "memory");
+}
 
 struct Frags {
   bf16x8 a[4], b[4];
@@ -506,34 +582,46 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
   // of LDS row 16 (8w + i) + lane / 4, i.e. row r0 + 16 i (r0 = 128 (w & 1) +
   // lane / 4) of this wave's operand: the history step for w < 2, the query
   // tile otherwise. swz of that row depends on lane and on i only via i % 2.
+  // swz of those rows is (lane / 16) % 4 for every i.
   const bool hist_side = w < 2;
   const int r0 = 128 * (w & 1) + (lane >> 2);
-  const uint32_t cb0 = (uint32_t)(((lane & 3) ^ swz(lane >> 2)) * 16);
-  const uint32_t cb1 = (uint32_t)(((lane & 3) ^ swz(16 + (lane >> 2))) * 16);
+  const uint32_t cb = (uint32_t)(((lane & 3) ^ swz(lane >> 2)) * 16);
   const uint32_t row_bytes = (uint32_t)d * 2u;
   int ld_step = 0, ld_kt = 0;
-  const char* src = nullptr;
-  int last = 0;
-  auto issue = [&](int g) {
-    if (ld_kt == 0) {                         // next step: new source rows
-      if (hist_side) {
-        const int base_row = h_first + ld_step * h_stride;
-        src = reinterpret_cast<const char*>(hist + (size_t)base_row * d);
-        last = N - 1 - base_row;
-      } else {
-        src = reinterpret_cast<const char*>(queries + (size_t)q0 * d);
-        last = Q - 1 - q0;
-      }
+  const char* src = nullptr;                  // source of slice ld_kt of step ld_step
+  uint32_t off[kLoads];                       // per-lane byte offsets within a slice
+  auto next_source = [&]() {                  // at the first slice of step ld_step
+    int last;
+    if (hist_side) {
+      const int base_row = h_first + ld_step * h_stride;
+      src = reinterpret_cast<const char*>(hist + (size_t)base_row * d);
+      last = N - 1 - base_row;
+    } else {
+      src = reinterpret_cast<const char*>(queries + (size_t)q0 * d);
+      last = Q - 1 - q0;
     }
-    const uint32_t m0 = lds0 + (uint32_t)((g & (kStages - 1)) * kStageBytes + w * kLoads * 1024);
-    const uint32_t kb = (uint32_t)ld_kt * (kKT * 2);
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const uint32_t off = (uint32_t)min(r0 + 16 * i, last) * row_bytes + ((i & 1) ? cb1 : cb0) + kb;
-      load_to_lds(src, off, m0 + i * 1024);
-    }
-    if (++ld_kt == nk) { ld_kt = 0; ++ld_step; }
+    for (int i = 0; i < kLoads; ++i) off[i] = (uint32_t)min(r0 + 16 * i, last) * row_bytes + cb;
   };
+  // Load i (0..7) of slice g into its stage; then advance to the next slice.
+  auto issue_one = [&](int g, int i, int enabled) {
+    const uint32_t m0 = lds0 + (uint32_t)((g % kStages) * kStageBytes + (w * kLoads + i) * 1024);
+    load_to_lds_if(src, off[i], __builtin_amdgcn_readfirstlane(m0), __builtin_amdgcn_readfirstlane(enabled));
+  };
+  auto advance = [&]() {
+    src += kKT * 2;
+    if (++ld_kt == nk) {
+      ld_kt = 0;
+      ++ld_step;
+      if (ld_step < n_steps) next_source();
+    }
+  };
+  auto issue = [&](int g) {
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) issue_one(g, i, 1);
+    advance();
+  };
+  next_source();
 
   // Operand reads: A = history rows 128 wh + 32 u + l32, B = query rows
   // 256 + 128 wq + 32 t + l32; k chunk 2 kk + half of the slice.
@@ -545,7 +633,7 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
     b_off[kk] = (uint32_t)((256 + 128 * wq + l32) * 64) + pos;
   }
   auto read = [&](int g, int kk, Frags& f) {
-    const char* stage = lds + (g & (kStages - 1)) * kStageBytes;
+    const char* stage = lds + (g % kStages) * kStageBytes;
 #pragma unroll
     for (int u = 0; u < 4; ++u) f.a[u] = *reinterpret_cast<const bf16x8*>(stage + a_off[kk] + u * 2048);
 #pragma unroll
@@ -555,9 +643,7 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
   __syncthreads();                              // earlier users of the LDS are done
   const int pre = min(kAhead, total);
   for (int g = 0; g < pre; ++g) issue(g);
-  if (pre == 3) wait_loads<2 * kLoads>();
-  else if (pre == 2) wait_loads<kLoads>();
-  else wait_loads<0>();
+  wait_slices(pre - 1);                         // slice 0 has landed
   barrier();
   Frags f0, f1;
   read(0, 0, f0);
@@ -578,13 +664,20 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
       } else {
         mma(acc, f0);
       }
-      // Slice g + 1 must have landed; slices up to min(total - 1, g + 2) are issued.
-      if (g + 2 < total) wait_loads<kLoads>();
-      else wait_loads<0>();
-      barrier();                                // also: all waves are done with stage (g - 1) % 4
-      if (g + kAhead < total) issue(g + kAhead);
+      // Slice g + 1 must have landed; slices up to min(total - 1, g + kAhead - 1) are issued.
+      wait_slices(min(total - 1, g + kAhead - 1) - (g + 1));
+      barrier();                                // also: all waves are done with stage (g - 1) % kStages
       if (g + 1 < total) read(g + 1, 0, f0);
-      mma(acc, f1);
+      // The loads of slice g + kAhead (if any) go out between the MFMAs.
+      const int more = g + kAhead < total;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[u], f1.b[t], acc[u][t], 0, 0, 0);
+          if ((4 * u + t) % 2 == 1) issue_one(g + kAhead, (4 * u + t) / 2, more);
+        }
+      if (more) advance();
       ++g;
     };
     slice(true);
@@ -646,13 +739,22 @@ __device__ __forceinline__ float pick_score(const floatx16 (&acc)[4][4], int t, 
 // count goes to seg_count[q][chunk] even when the segment overflows.
 __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
     const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
-    int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0, int seg_cap,
-    uint64_t* __restrict__ seg, int* __restrict__ seg_count) {
+    int chunk_rows, int n_chunks, int q_tiles, int q_groups, const float* __restrict__ theta0,
+    int seg_cap, uint64_t* __restrict__ seg, int* __restrict__ seg_count) {
   __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
   __shared__ int cnt[ring::kBQ];
   int qt, chunk;
   const int b = blockIdx.x;
-  if (n_chunks % 8 == 0) {
+  if (q_groups > 0) {
+    // Workgroup b runs on XCD b % 8. XCD x owns query-tile group x % q_groups
+    // and chunk group x / q_groups: its L2 keeps that group's query tiles
+    // resident while the chunks stream through.
+    const int x = b & 7, slot = b >> 3;
+    const int per_group = q_tiles / q_groups;
+    const int chunks_per_group = n_chunks / (8 / q_groups);
+    qt = (x % q_groups) * per_group + slot % per_group;
+    chunk = (x / q_groups) * chunks_per_group + slot / per_group;
+  } else if (n_chunks % 8 == 0) {
     const int x = b & 7, slot = b >> 3;
     chunk = x + 8 * (slot / q_tiles);
     qt = slot % q_tiles;
@@ -716,13 +818,6 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
   if (q0 + tid < Q) seg_count[(size_t)(q0 + tid) * n_chunks + chunk] = cnt[tid];
 }
 
-// Descending order of a bitonic sequence held one key per lane (half-cleaners).
-__device__ __forceinline__ uint64_t wave_bitonic_clean_desc64(uint64_t v) {
-#pragma unroll
-  for (int stride = 32; stride > 0; stride >>= 1) v = cx_lanes(v, stride, true);
-  return v;
-}
-
 // Select kernel: one workgroup (4 waves) per query. Candidate p of the
 // query's concatenated segments is found by a search of the segment offsets
 // and read straight from global memory, 64 at a time per wave. Each wave keeps
@@ -764,33 +859,27 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
   if (tid == 0) flags[q] = 0;
   const int total = off[kWave];
   const uint64_t* src = seg + (size_t)q * n_chunks * seg_cap;
-  uint64_t list = kPadKey;
-  for (int base = w * kWave; base < total; base += 4 * kWave) {
-    const int p = base + lane;
-    uint64_t key = kPadKey;
-    if (p < total) {
-      int lo = 0, hi = n_chunks - 1;                  // last segment with off <= p
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (off[mid] <= p) lo = mid;
-        else hi = mid - 1;
-      }
-      key = src[(size_t)lo * seg_cap + (p - off[lo])];
+  auto candidate = [&](int p) -> uint64_t {
+    if (p >= total) return kPadKey;
+    int lo = 0, hi = n_chunks - 1;                    // last segment with off <= p
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= p) lo = mid;
+      else hi = mid - 1;
     }
-    const uint64_t last = shfl_u64(list, kWave - 1);
-    if (!__any(key > last)) continue;
-    key = wave_sort_desc64(key);
-    const uint64_t rev = shfl_u64(key, kWave - 1 - lane);
-    list = wave_bitonic_clean_desc64(list > rev ? list : rev);
+    return src[(size_t)lo * seg_cap + (p - off[lo])];
+  };
+  uint64_t list = kPadKey;
+  uint64_t next = candidate(w * kWave + lane);
+  for (int base = w * kWave; base < total; base += 4 * kWave) {
+    const uint64_t cur = next;
+    next = candidate(base + 4 * kWave + lane);        // prefetch
+    list = fold_group(list, cur);
   }
   lists[w][lane] = list;
   __syncthreads();
   if (w != 0) return;
-#pragma unroll
-  for (int o = 1; o < 4; ++o) {
-    const uint64_t other = lists[o][kWave - 1 - lane];
-    list = wave_bitonic_clean_desc64(list > other ? list : other);
-  }
+  list = fold_lists(list, lists);
   if (lane < k) {
     ids[(size_t)q * k + lane] = list == kPadKey ? -1 : key_id(list);
     sims[(size_t)q * k + lane] = list == kPadKey ? -__builtin_inff() : key_sim(list);
@@ -828,11 +917,15 @@ hipError_t launch_theta(const uint16_t* queries, int Q, const uint16_t* hist, in
     }
   }
   const int m = p.n_samples * 16;
-  int m2 = 1;
-  while (m2 < m) m2 <<= 1;
   LaunchScope scope("threshold_select", stream);
-  hipLaunchKernelGGL(threshold_select_kernel, dim3(Q), dim3(256), m2 * sizeof(float), stream, gm, m,
-                     m2, k, theta0);
+  if (k <= kWave) {
+    hipLaunchKernelGGL(threshold_select64_kernel, dim3(Q), dim3(256), 0, stream, gm, m, k, theta0);
+  } else {
+    int m2 = 1;
+    while (m2 < m) m2 <<= 1;
+    hipLaunchKernelGGL(threshold_select_kernel, dim3(Q), dim3(256), m2 * sizeof(float), stream, gm, m,
+                       m2, k, theta0);
+  }
   return hipGetLastError();
 }
 
@@ -854,7 +947,6 @@ void chunking(int q_tiles, int N, int target_blocks, int max_chunks, int* chunk_
 }  // namespace
 
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
-  (void)d;
   SimTopkPlan p{};
   int L = 64;
   while (L < k) L <<= 1;
@@ -862,12 +954,15 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   p.q_tile = L == 64 ? 128 : (L == 128 ? 64 : 32);
   p.q_tiles = (Q + p.q_tile - 1) / p.q_tile;
   chunking(p.q_tiles, N, 1024, 1 << 20, &p.chunk_rows, &p.n_chunks);
-  // Threshold pre-pass: every SR-th step, >= 4k group maxima, at most 8192, SR <= 32.
+  // Threshold pre-pass: every SR-th step, >= 4k group maxima, at most 8192.
+  // SR <= 16 on the filtered path (every candidate above theta0 is written
+  // out there, so a tighter bound pays for the larger sample), else <= 32.
   // Only whole steps are sampled.
   const long steps = (long)N / kStepRows;
   if (steps * 16 >= 8L * k) {
+    const long sr_max = L == 64 ? 16 : 32;
     long sr = steps * 16 / (4L * k);
-    if (sr > 32) sr = 32;
+    if (sr > sr_max) sr = sr_max;
     if (sr < 1) sr = 1;
     while ((steps + sr - 1) / sr > 512) ++sr;
     p.sample_every = (int)sr;
@@ -882,6 +977,13 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
     while (p.n_samples > 0 && (long)p.f_q_tiles * ((p.n_samples + 2 * p.f_spb - 1) / (2 * p.f_spb)) >= 256)
       p.f_spb *= 2;
     chunking(p.f_q_tiles, N, 512, 64, &p.f_chunk_rows, &p.f_n_chunks);
+    // Query-tile groups per XCD: the fewest (of 1, 2, 4, 8) whose tiles take at
+    // most 2 MiB of an XCD's 4 MiB L2 (0: no grouping).
+    p.f_q_groups = 0;
+    for (int a = 1; a <= 8; a *= 2) {
+      if (p.f_q_tiles % a != 0 || p.f_n_chunks % (8 / a) != 0) continue;
+      if ((size_t)(p.f_q_tiles / a) * ring::kBQ * d * 2 <= ((size_t)2 << 20)) { p.f_q_groups = a; break; }
+    }
     p.seg_cap = 1;                                   // power of two, n_chunks * cap <= 8192
     while (p.seg_cap * 2 * p.f_n_chunks <= 8192) p.seg_cap *= 2;
   }
@@ -918,7 +1020,7 @@ hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* his
     {
       LaunchScope scope("sim_topk", stream);
       hipLaunchKernelGGL(sim_filter_kernel, dim3(p.f_q_tiles * p.f_n_chunks), dim3(kThreads), 0, stream,
-                         queries, Q, hist, N, d, p.f_chunk_rows, p.f_n_chunks, p.f_q_tiles,
+                         queries, Q, hist, N, d, p.f_chunk_rows, p.f_n_chunks, p.f_q_tiles, p.f_q_groups,
                          p.n_samples > 0 ? theta0 : nullptr, p.seg_cap, seg, segcnt);
     }
     {

@@ -34,6 +34,7 @@ struct SimTopkPlan {
   bool fast;
   int f_q_tiles, f_chunk_rows, f_n_chunks;
   int f_spb;        // sampled steps per threshold-sampling workgroup
+  int f_q_groups;   // query-tile groups across the 8 XCDs (0: plain mapping)
   int seg_cap;      // candidate keys per (query, chunk) segment
   // workspace layout (byte offsets, 256-aligned)
   size_t off_partial, off_gm, off_theta, off_seg, off_segcnt, off_flags, total_bytes;
