@@ -68,6 +68,11 @@ def read_traffic(kernel: str, workload_key: str):
         return None
 
 
+def kernel_name(k: int) -> str:
+    """The kernel behind the `sim_topk` timer label: the filtered path for k <= 64."""
+    return "sim_filter_kernel" if k <= 64 else "sim_topk_kernel"
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle (as it stands) on a bounded sample of the same batch."""
     import oracle
@@ -171,7 +176,7 @@ def main():
     k1_avg_s = k1_ms / n_launch / 1e3
     flops = 2.0 * Q * N * d
     achieved = flops / k1_avg_s / 1e12
-    workload_key = f"config{args.config}"
+    workload_key = workloads.WORKLOAD_NAMES[args.config].split(":")[0]
     traffic = read_traffic("sim_topk", workload_key)
 
     line = {
@@ -189,7 +194,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": workloads.WORKLOAD_NAMES[args.config], "Q": Q, "N": N, "d": d,
                    "k": k, "B": B, "tau": spec.tau, "seed": w.seed},
-        "roofline": {"bound": "mfma", "kernel": "sim_topk", "achieved": achieved,
+        "roofline": {"bound": "mfma", "kernel": kernel_name(k), "achieved": achieved,
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
                      "avg_launch_us": k1_avg_s * 1e6, "flops_per_launch": flops},
