@@ -257,6 +257,38 @@ __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
   }
 }
 
+// Rank of a small queue (Q <= kRankSmallMax) in one workgroup: keys
+// (monotone index bits << 32 | request id) are unique, so a bitonic sort in
+// LDS is the stable ascending order. One launch instead of twelve.
+constexpr int kRankSmallMax = 16384;
+
+__global__ void __launch_bounds__(1024) rank_small_kernel(const float* __restrict__ g_in, int Q,
+                                                          int32_t* __restrict__ order) {
+  __shared__ uint64_t keys[kRankSmallMax];
+  int n2 = 2;
+  while (n2 < Q) n2 <<= 1;
+  for (int i = threadIdx.x; i < n2; i += 1024)
+    keys[i] = i < Q ? ((uint64_t)index_key(g_in[i]) << 32) | (uint32_t)i : ~0ull;
+  __syncthreads();
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int ls = __builtin_ctz((unsigned)size) - 1; ls >= 0; --ls) {
+      const int stride = 1 << ls;
+      for (int e = threadIdx.x; e < n2 / 2; e += 1024) {
+        const int i = ((e >> ls) << (ls + 1)) | (e & (stride - 1));
+        const int j = i + stride;
+        const bool asc = (i & size) == 0;
+        const uint64_t a = keys[i], b = keys[j];
+        if ((a > b) == asc) {
+          keys[i] = b;
+          keys[j] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < Q; i += 1024) order[i] = (int32_t)(uint32_t)keys[i];
+}
+
 }  // namespace
 
 size_t rank_workspace_bytes(int Q) {
@@ -282,6 +314,11 @@ hipError_t launch_index(const float* mass, const float* cost, const int32_t* pro
 
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
+  if (Q <= kRankSmallMax) {
+    LaunchScope scope("rank_small", stream);
+    hipLaunchKernelGGL(rank_small_kernel, dim3(1), dim3(1024), 0, stream, index, Q, order);
+    return hipGetLastError();
+  }
   const int n_tiles = (Q + kRankTile - 1) / kRankTile;
   uint32_t* kA = static_cast<uint32_t*>(ws);
   uint32_t* vA = kA + Q;

@@ -160,17 +160,34 @@ def _cluster_probs(spec: PredictSpec, rng) -> np.ndarray:
 
 
 def _points(rng, centres, assign, spec: PredictSpec, noise_mask, block=65536) -> np.ndarray:
+    """Unit rows around the assigned centres (noise rows: uniform on the sphere).
+
+    Block i of `block` rows draws from its own child of rng's seed sequence, so
+    the blocks are generated in parallel threads and the result does not depend
+    on the thread count.
+    """
+    import os
+    from concurrent.futures import ThreadPoolExecutor
     n, d = assign.shape[0], centres.shape[1]
     out = np.empty((n, d), dtype=np.float32)
-    scale = spec.sigma if spec.sigma_per_coordinate else spec.sigma / np.sqrt(d)
-    for s in range(0, n, block):
-        e = min(n, s + block)
-        g = rng.standard_normal((e - s, d))
-        a = assign[s:e]
+    scale = np.float32(spec.sigma if spec.sigma_per_coordinate else spec.sigma / np.sqrt(d))
+    c32 = centres.astype(np.float32)
+    n_blocks = (n + block - 1) // block
+    kids = rng.bit_generator.seed_seq.spawn(n_blocks)
+
+    def work(i):
+        s, e = i * block, min(n, (i + 1) * block)
+        g = np.random.default_rng(kids[i]).standard_normal((e - s, d), dtype=np.float32)
+        x = c32[np.maximum(assign[s:e], 0)]
+        x += scale * g
         nm = noise_mask[s:e]
-        x = centres[np.maximum(a, 0)] + scale * g
         x[nm] = g[nm]                       # uniform on the sphere after normalising
-        out[s:e] = _unit_rows(x).astype(np.float32)
+        x /= np.linalg.norm(x, axis=1, keepdims=True)
+        out[s:e] = x
+
+    threads = max(1, min(16, os.cpu_count() or 1, n_blocks))
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(work, range(n_blocks)))
     return out
 
 

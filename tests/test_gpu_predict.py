@@ -137,3 +137,23 @@ def test_config2_full_size_sampled():
     parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
     parity.check_rank(order, g)
     print(f"config 2: {equal}/{len(rows)} sampled queries with the exact neighbour set", flush=True)
+
+
+def test_config3_full_size_sampled():
+    """The GEMM-bound workload (1M rows, d = 1024, 10% noise rows and queries), sampled."""
+    w = workloads.make_config(3)
+    spec = w.spec
+    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
+                       spec.k, spec.tau)
+    out = store.decide(dev(w.queries), dev(w.prompt_len))
+    ids, sims, counts, mass, g, order = [host(t) for t in out]
+    rng = np.random.default_rng(3)
+    noise_q = np.nonzero(w.query_cluster < 0)[0]
+    rows = np.concatenate([rng.choice(spec.Q, size=20, replace=False), noise_q[:4], [0, spec.Q - 1]])
+    rows = np.unique(rows)
+    S = oracle_scores(w, rows)
+    equal = parity.check_topk(ids[rows], sims[rows], S, spec.k)
+    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
+    parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
+    parity.check_rank(order, g)
+    print(f"config 3: {equal}/{len(rows)} sampled queries with the exact neighbour set", flush=True)

@@ -101,7 +101,7 @@ def test_index_config4_full():
 
 
 # ------------------------------------------------------------------ rank
-@pytest.mark.parametrize("Q", [1, 2, 2047, 2048, 2049, 5000, 65536, 131073])
+@pytest.mark.parametrize("Q", [1, 2, 3, 2047, 2048, 2049, 5000, 16384, 16385, 65536, 131073])
 def test_rank_bit_exact(Q):
     rng = np.random.default_rng(Q)
     g = np.round(rng.uniform(0, 50, size=Q)).astype(np.float32)   # many exact ties
