@@ -221,31 +221,6 @@ __global__ void __launch_bounds__(kThreads, 1) threshold_sample_kernel(
   }
 }
 
-// theta0[q] = k-th largest of the query's m group maxima (-inf when fewer
-// than k exist): bitonic sort in LDS, one workgroup per query.
-__global__ void __launch_bounds__(256) threshold_select_kernel(const float* __restrict__ gm, int m,
-                                                               int m_pow2, int k,
-                                                               float* __restrict__ theta0) {
-  extern __shared__ float vals[];
-  const int q = blockIdx.x;
-  const float* src = gm + (size_t)q * m;
-  for (int i = threadIdx.x; i < m_pow2; i += 256) vals[i] = i < m ? src[i] : -__builtin_inff();
-  __syncthreads();
-  for (int size = 2; size <= m_pow2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int e = threadIdx.x; e < m_pow2 / 2; e += 256) {
-        const int i = (e / stride) * (2 * stride) + (e % stride);
-        const int j = i + stride;
-        const bool desc = (i & size) == 0;
-        const float a = vals[i], b = vals[j];
-        if ((a < b) == desc) { vals[i] = b; vals[j] = a; }
-      }
-      __syncthreads();
-    }
-  }
-  if (threadIdx.x == 0) theta0[q] = k <= m ? vals[k - 1] : -__builtin_inff();
-}
-
 // ------------------------------------------------------------------------
 // Main kernel.
 // ------------------------------------------------------------------------
@@ -458,29 +433,62 @@ __device__ __forceinline__ uint64_t fold_lists(uint64_t list, const uint64_t (&l
   return list;
 }
 
-// theta0 for k <= 64: the k-th largest of a query's m group maxima, with
-// per-wave top-64 lists in registers (keys: maximum, then position).
-__global__ void __launch_bounds__(256) threshold_select64_kernel(const float* __restrict__ gm, int m, int k,
-                                                                 float* __restrict__ theta0) {
-  __shared__ uint64_t lists[4][kWave];
+// theta0: the k-th largest of a query's m (<= kMaxSamples * 16) group maxima,
+// found by a radix select on their monotone bits, one 8-bit digit per pass
+// from the top: count the values that match the digits fixed so far per next
+// digit (LDS atomics), then fix the digit whose suffix count reaches the rank
+// still wanted. Exact: the result is the k-th largest value itself.
+constexpr int kMaxGroupMaxima = 512 * 16;
+
+__global__ void __launch_bounds__(256) threshold_radix_kernel(const float* __restrict__ gm, int m, int k,
+                                                              float* __restrict__ theta0) {
+  __shared__ uint32_t vals[kMaxGroupMaxima];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t pick[2];                        // digit, count of values above it
   const int q = blockIdx.x;
-  const int lane = (int)lane_id();
-  const int w = threadIdx.x / kWave;
+  const int t = threadIdx.x;
   const float* src = gm + (size_t)q * m;
-  uint64_t list = kPadKey;
-  int p = w * kWave + lane;
-  uint64_t next = p < m ? make_key(src[p], (uint32_t)p) : kPadKey;
-  for (int base = w * kWave; base < m; base += 4 * kWave) {
-    const uint64_t cur = next;
-    p = base + 4 * kWave + lane;
-    next = p < m ? make_key(src[p], (uint32_t)p) : kPadKey;     // prefetch
-    list = fold_group(list, cur);
+  for (int i = t; i < m; i += 256) vals[i] = f32_order_bits(src[i]);
+  if (t < 2) pick[t] = 0;
+  uint32_t prefix = 0, mask = 0;
+  int want = k;                                       // rank wanted among the matching values
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    hist[t] = 0;
+    __syncthreads();
+    for (int i = t; i < m; i += 256) {
+      const uint32_t v = vals[i];
+      if ((v & mask) == prefix) atomicAdd(&hist[(v >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (t < kWave) {                                  // suffix counts over the 256 digits
+      uint32_t c[4], run = 0;
+#pragma unroll
+      for (int j = 3; j >= 0; --j) { run += hist[4 * t + j]; c[j] = run; }   // within lane, high first
+      uint32_t above = 0;                             // sum of hist over lanes > t
+      {
+        uint32_t x = run;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint32_t y = __shfl_down(x, o, kWave);
+          if (t + o < kWave) x += y;
+        }
+        above = x - run;
+      }
+      // digit 4t + j has (above + c[j]) values >= it and (above + c[j] - hist) above it
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t ge = above + c[j];
+        const uint32_t gt = ge - hist[4 * t + j];
+        if (gt < (uint32_t)want && ge >= (uint32_t)want) { pick[0] = 4 * t + j; pick[1] = gt; }
+      }
+    }
+    __syncthreads();
+    prefix |= pick[0] << shift;
+    mask |= 255u << shift;
+    want -= (int)pick[1];
+    __syncthreads();
   }
-  lists[w][lane] = list;
-  __syncthreads();
-  if (w != 0) return;
-  list = fold_lists(list, lists);
-  if (lane == k - 1) theta0[q] = k <= m ? key_sim(list) : -__builtin_inff();
+  if (t == 0) theta0[q] = k <= m ? f32_from_order_bits(prefix) : -__builtin_inff();
 }
 
 // ========================================================================
@@ -918,14 +926,7 @@ hipError_t launch_theta(const uint16_t* queries, int Q, const uint16_t* hist, in
   }
   const int m = p.n_samples * 16;
   LaunchScope scope("threshold_select", stream);
-  if (k <= kWave) {
-    hipLaunchKernelGGL(threshold_select64_kernel, dim3(Q), dim3(256), 0, stream, gm, m, k, theta0);
-  } else {
-    int m2 = 1;
-    while (m2 < m) m2 <<= 1;
-    hipLaunchKernelGGL(threshold_select_kernel, dim3(Q), dim3(256), m2 * sizeof(float), stream, gm, m,
-                       m2, k, theta0);
-  }
+  hipLaunchKernelGGL(threshold_radix_kernel, dim3(Q), dim3(256), 0, stream, gm, m, k, theta0);
   return hipGetLastError();
 }
 
@@ -989,6 +990,8 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   }
   size_t o = 0;
   p.off_partial = o; o = align256(o + (size_t)Q * p.n_chunks * L * sizeof(uint64_t));
+  const int groups = merge_groups(Q, p.n_chunks, L);
+  p.off_merge = o;   o = align256(o + (groups > 1 ? (size_t)Q * groups * L * sizeof(uint64_t) : 0));
   p.off_gm = o;      o = align256(o + (size_t)Q * p.n_samples * 16 * sizeof(float));
   p.off_theta = o;   o = align256(o + (size_t)Q * sizeof(float));
   if (p.fast) {
@@ -1006,6 +1009,7 @@ hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* his
   if (Q == 0) return hipSuccess;
   char* ws = static_cast<char*>(workspace);
   uint64_t* partial = reinterpret_cast<uint64_t*>(ws + p.off_partial);
+  uint64_t* merge_lists = reinterpret_cast<uint64_t*>(ws + p.off_merge);
   float* gm = reinterpret_cast<float*>(ws + p.off_gm);
   float* theta0 = reinterpret_cast<float*>(ws + p.off_theta);
   hipError_t e;
@@ -1031,7 +1035,7 @@ hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* his
     // Exact fallback for queries whose candidates overflowed (no work otherwise).
     e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
     if (e != hipSuccess) return e;
-    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, ids, sims, stream);
+    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, merge_lists, ids, sims, stream);
   }
   if (p.n_samples > 0) {
     e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, false, gm, theta0, stream);
@@ -1041,7 +1045,7 @@ hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* his
   if (p.list_len == 128) e = launch_lists<2, 128>(queries, Q, hist, N, d, k, p, th, nullptr, partial, stream);
   else e = launch_lists<1, 256>(queries, Q, hist, N, d, k, p, th, nullptr, partial, stream);
   if (e != hipSuccess) return e;
-  return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, nullptr, ids, sims, stream);
+  return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, nullptr, merge_lists, ids, sims, stream);
 }
 
 }  // namespace sage

@@ -15,21 +15,28 @@ namespace {
 constexpr int kMergeThreads = 256;
 constexpr int kMergeKeys = 4096;   // LDS capacity in keys (32 KiB)
 
+// Workgroup (q, y) merges lists [y * per_group, ...) of query q (all of them
+// when gridDim.y == 1). With `out_lists` it writes the merged list of L keys
+// to out_lists[q][y] (first level of a two-level merge); otherwise the first
+// k entries as ids and similarities.
 __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
-    const uint64_t* __restrict__ partial, int n_lists, int list_len, int k,
-    const int* __restrict__ only_flagged, int32_t* __restrict__ ids, float* __restrict__ sims) {
+    const uint64_t* __restrict__ partial, int n_lists, int list_len, int k, int per_group,
+    const int* __restrict__ only_flagged, uint64_t* __restrict__ out_lists, int32_t* __restrict__ ids,
+    float* __restrict__ sims) {
   __shared__ uint64_t slot[kMergeKeys];
   const int q = blockIdx.x;
   if (only_flagged && only_flagged[q] == 0) return;
   const int L = list_len;
   const int G = kMergeKeys / L;                 // lists per LDS batch (power of two)
-  const uint64_t* src = partial + (size_t)q * n_lists * L;
+  const int first = blockIdx.y * per_group;
+  const int count = min(per_group, n_lists - first);
+  const uint64_t* src = partial + ((size_t)q * n_lists + first) * L;
   const int t = threadIdx.x;
 
   bool have_result = false;
-  for (int base = 0; base < n_lists || !have_result;) {
+  for (int base = 0; base < count || !have_result;) {
     const int s0 = have_result ? 1 : 0;
-    const int n_load = min(G - s0, n_lists - base);
+    const int n_load = min(G - s0, count - base);
     int n_used = s0 + n_load;
     int n_tree = 1;
     while (n_tree < n_used) n_tree <<= 1;
@@ -62,6 +69,11 @@ __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
     have_result = true;
     base += n_load;
   }
+  if (out_lists) {
+    uint64_t* dst = out_lists + ((size_t)q * gridDim.y + blockIdx.y) * L;
+    for (int i = t; i < L; i += kMergeThreads) dst[i] = slot[i];
+    return;
+  }
   for (int i = t; i < k; i += kMergeThreads) {
     const uint64_t key = slot[i];
     ids[(size_t)q * k + i] = key == kPadKey ? -1 : key_id(key);
@@ -72,12 +84,29 @@ __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
 }  // namespace
 
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
-                             const int* only_flagged, int32_t* ids, float* sims, hipStream_t stream) {
+                             const int* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
+                             hipStream_t stream) {
   if (Q == 0) return hipSuccess;
   LaunchScope scope(only_flagged ? "topk_merge_fallback" : "topk_merge", stream);
-  hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, partial, n_lists,
-                     list_len, k, only_flagged, ids, sims);
+  const int groups = merge_groups(Q, n_lists, list_len);
+  if (groups > 1 && scratch_lists) {
+    // Few queries with many lists: merge groups of lists in parallel first.
+    const int per_group = (n_lists + groups - 1) / groups;
+    hipLaunchKernelGGL(topk_merge_kernel, dim3(Q, groups), dim3(kMergeThreads), 0, stream, partial,
+                       n_lists, list_len, k, per_group, only_flagged, scratch_lists, nullptr, nullptr);
+    hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, scratch_lists, groups,
+                       list_len, k, groups, only_flagged, nullptr, ids, sims);
+  } else {
+    hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, partial, n_lists,
+                       list_len, k, n_lists, only_flagged, nullptr, ids, sims);
+  }
   return hipGetLastError();
+}
+
+int merge_groups(int Q, int n_lists, int list_len) {
+  const int per_batch = kMergeKeys / list_len;
+  if (Q >= 1024 || n_lists <= per_batch) return 1;
+  return (n_lists + per_batch - 1) / per_batch;   // one LDS batch of lists per first-level group
 }
 
 }  // namespace sage

@@ -37,7 +37,7 @@ struct SimTopkPlan {
   int f_q_groups;   // query-tile groups across the 8 XCDs (0: plain mapping)
   int seg_cap;      // candidate keys per (query, chunk) segment
   // workspace layout (byte offsets, 256-aligned)
-  size_t off_partial, off_gm, off_theta, off_seg, off_segcnt, off_flags, total_bytes;
+  size_t off_partial, off_merge, off_gm, off_theta, off_seg, off_segcnt, off_flags, total_bytes;
   size_t workspace_bytes() const { return total_bytes; }
 };
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
@@ -57,8 +57,11 @@ hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* his
                              const SimTopkPlan& plan, void* workspace, int32_t* ids, float* sims,
                              hipStream_t stream);
 // Merge of per-chunk lists; with `only_flagged`, queries whose flag is 0 are skipped.
+// Number of first-level groups of the list merge (1: single level).
+int merge_groups(int Q, int n_lists, int list_len);
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
-                             const int* only_flagged, int32_t* ids, float* sims, hipStream_t stream);
+                             const int* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
+                             hipStream_t stream);
 hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, const int32_t* hist_len,
                        int N, float tau, const double* edges, int B, int32_t* counts, float* mass,
                        hipStream_t stream);

@@ -45,6 +45,8 @@ CASES = [
     (33, 2500, 64, 256, 1024),
     (5, 300, 64, 1, 7),
     (3, 10, 64, 32, 16),        # N < k: padded with -1 / -inf
+    (8, 300000, 64, 128, 512),  # few queries, hundreds of chunk lists: two-level merge
+    (8, 200000, 32, 200, 64),
 ]
 
 
