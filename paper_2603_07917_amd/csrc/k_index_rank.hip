@@ -257,36 +257,122 @@ __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
   }
 }
 
-// Rank of a small queue (Q <= kRankSmallMax) in one workgroup: keys
-// (monotone index bits << 32 | request id) are unique, so a bitonic sort in
-// LDS is the stable ascending order. One launch instead of twelve.
+// Rank of a small queue (Q <= kRankSmallMax) in one workgroup of 1024
+// threads: the same stable LSD radix sort (8-bit digits, 4 passes), with the
+// keys and request ids kept in registers and scattered through LDS. Element
+// e = 1024 r + t is item r of thread t, so rounds r run in index order. Per
+// pass: digit totals (wave ballots), their exclusive scan, then per round the
+// per-wave digit counts and a stable scatter.
 constexpr int kRankSmallMax = 16384;
+constexpr int kRankSmallThreads = 1024;
+constexpr int kRankSmallItems = kRankSmallMax / kRankSmallThreads;
 
-__global__ void __launch_bounds__(1024) rank_small_kernel(const float* __restrict__ g_in, int Q,
-                                                          int32_t* __restrict__ order) {
-  __shared__ uint64_t keys[kRankSmallMax];
-  int n2 = 2;
-  while (n2 < Q) n2 <<= 1;
-  for (int i = threadIdx.x; i < n2; i += 1024)
-    keys[i] = i < Q ? ((uint64_t)index_key(g_in[i]) << 32) | (uint32_t)i : ~0ull;
+__global__ void __launch_bounds__(kRankSmallThreads) rank_small_kernel(const float* __restrict__ g_in, int Q,
+                                                                       int32_t* __restrict__ order) {
+  constexpr int kWaves = kRankSmallThreads / kWave;
+  __shared__ uint32_t kbuf[kRankSmallMax];
+  __shared__ uint32_t vbuf[kRankSmallMax];
+  __shared__ uint32_t wave_cnt[kWaves][256];
+  __shared__ uint32_t base[256];
+  const int t = threadIdx.x;
+  const int lane = (int)lane_id();
+  const int w = t / kWave;
+  const int rounds = (Q + kRankSmallThreads - 1) / kRankSmallThreads;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  uint32_t key[kRankSmallItems], val[kRankSmallItems];
+#pragma unroll
+  for (int r = 0; r < kRankSmallItems; ++r) {
+    const int e = r * kRankSmallThreads + t;
+    key[r] = e < Q ? index_key(g_in[e]) : 0u;
+    val[r] = (uint32_t)e;
+  }
+  for (int i = t; i < kWaves * 256; i += kRankSmallThreads) (&wave_cnt[0][0])[i] = 0;
   __syncthreads();
-  for (int size = 2; size <= n2; size <<= 1) {
-    for (int ls = __builtin_ctz((unsigned)size) - 1; ls >= 0; --ls) {
-      const int stride = 1 << ls;
-      for (int e = threadIdx.x; e < n2 / 2; e += 1024) {
-        const int i = ((e >> ls) << (ls + 1)) | (e & (stride - 1));
-        const int j = i + stride;
-        const bool asc = (i & size) == 0;
-        const uint64_t a = keys[i], b = keys[j];
-        if ((a > b) == asc) {
-          keys[i] = b;
-          keys[j] = a;
-        }
+  for (int shift = 0; shift < 32; shift += 8) {
+    // digit totals (wave_cnt is all zero here)
+#pragma unroll
+    for (int r = 0; r < kRankSmallItems; ++r) {
+      if (r >= rounds) break;
+      const bool valid = r * kRankSmallThreads + t < Q;
+      const uint32_t digit = (key[r] >> shift) & 255u;
+      uint64_t peers = __ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const bool on = (digit >> bit) & 1u;
+        const uint64_t m = __ballot(on);
+        peers &= on ? m : ~m;
+      }
+      if (valid && __popcll(peers & lt_mask) == 0) wave_cnt[w][digit] += (uint32_t)__popcll(peers);
+    }
+    __syncthreads();
+    if (t < 256) {                                     // read and clear column t
+      uint32_t tot = 0;
+#pragma unroll
+      for (int i = 0; i < kWaves; ++i) { tot += wave_cnt[i][t]; wave_cnt[i][t] = 0; }
+      base[t] = tot;
+    }
+    __syncthreads();
+    if (t < kWave) {                                   // exclusive scan of 256 totals, 4 per lane
+      uint32_t c[4], run = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { c[j] = run; run += base[4 * t + j]; }
+      uint32_t incl = run;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      const uint32_t before = incl - run;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) base[4 * t + j] = before + c[j];
+    }
+    __syncthreads();
+    // stable scatter, round by round
+#pragma unroll
+    for (int r = 0; r < kRankSmallItems; ++r) {
+      if (r >= rounds) break;
+      const bool valid = r * kRankSmallThreads + t < Q;
+      const uint32_t digit = (key[r] >> shift) & 255u;
+      uint64_t peers = __ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const bool on = (digit >> bit) & 1u;
+        const uint64_t m = __ballot(on);
+        peers &= on ? m : ~m;
+      }
+      const uint32_t rank_in_wave = (uint32_t)__popcll(peers & lt_mask);
+      if (valid && rank_in_wave == 0) wave_cnt[w][digit] = (uint32_t)__popcll(peers);
+      __syncthreads();
+      if (valid) {
+        uint32_t pos = base[digit] + rank_in_wave;
+        for (int i = 0; i < w; ++i) pos += wave_cnt[i][digit];
+        kbuf[pos] = key[r];
+        vbuf[pos] = val[r];
+      }
+      __syncthreads();
+      if (t < 256) {                                   // advance column t, clear it for the next round
+        uint32_t add = 0;
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i) { add += wave_cnt[i][t]; wave_cnt[i][t] = 0; }
+        base[t] += add;
       }
       __syncthreads();
     }
+#pragma unroll
+    for (int r = 0; r < kRankSmallItems; ++r) {
+      const int e = r * kRankSmallThreads + t;
+      if (e < Q) {
+        key[r] = kbuf[e];
+        val[r] = vbuf[e];
+      }
+    }
+    __syncthreads();
   }
-  for (int i = threadIdx.x; i < Q; i += 1024) order[i] = (int32_t)(uint32_t)keys[i];
+#pragma unroll
+  for (int r = 0; r < kRankSmallItems; ++r) {
+    const int e = r * kRankSmallThreads + t;
+    if (e < Q) order[e] = (int32_t)val[r];
+  }
 }
 
 }  // namespace
@@ -316,7 +402,7 @@ hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipS
   if (Q == 0) return hipSuccess;
   if (Q <= kRankSmallMax) {
     LaunchScope scope("rank_small", stream);
-    hipLaunchKernelGGL(rank_small_kernel, dim3(1), dim3(1024), 0, stream, index, Q, order);
+    hipLaunchKernelGGL(rank_small_kernel, dim3(1), dim3(kRankSmallThreads), 0, stream, index, Q, order);
     return hipGetLastError();
   }
   const int n_tiles = (Q + kRankTile - 1) / kRankTile;

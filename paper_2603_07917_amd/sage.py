@@ -247,6 +247,66 @@ class Store:
         return ids, sims, counts, mass, g, order
 
 
+class Queue:
+    """A standing queue of pending requests, re-ranked at every decision.
+
+    Each slot holds one pending request's length distribution (mass) and
+    prompt length. A decision predicts the new arrivals into the slots freed by
+    the previous dispatch, re-indexes every slot, ranks them and dispatches the
+    first `batch` (smallest index first), whose slots take the next arrivals.
+    Buffers are allocated once; the per-decision bookkeeping (slot refills) is
+    plain tensor indexing.
+    """
+
+    def __init__(self, store: Store, mass: torch.Tensor, prompt_len: torch.Tensor, batch: int):
+        _dev(mass, torch.float32, "mass", 2)
+        _dev(prompt_len, torch.int32, "prompt_len", 1)
+        n0, B = mass.shape
+        dev = mass.device
+        self.store = store
+        self.batch = int(batch)
+        self.slots = n0 + self.batch
+        self.mass = torch.zeros((self.slots, B), dtype=torch.float32, device=dev)
+        self.mass[:n0] = mass
+        self.prompt_len = torch.ones(self.slots, dtype=torch.int32, device=dev)
+        self.prompt_len[:n0] = prompt_len
+        self.request = torch.full((self.slots,), -1, dtype=torch.int64, device=dev)
+        self.request[:n0] = torch.arange(n0, dtype=torch.int64, device=dev)
+        self.next_request = n0
+        self.free = torch.arange(n0, self.slots, dtype=torch.int64, device=dev)
+        self.index = torch.empty(self.slots, dtype=torch.float32, device=dev)
+        self.order = torch.empty(self.slots, dtype=torch.int32, device=dev)
+        self._rank_ws = torch.empty(max(16, rank_workspace_bytes(self.slots)), dtype=torch.uint8,
+                                    device=dev)
+        k = store.k
+        self._pred = (torch.empty((self.batch, k), dtype=torch.int32, device=dev),
+                      torch.empty((self.batch, k), dtype=torch.float32, device=dev),
+                      torch.empty((self.batch, B), dtype=torch.int32, device=dev),
+                      torch.empty((self.batch, B), dtype=torch.float32, device=dev))
+        self._arange = torch.arange(self.batch, dtype=torch.int64, device=dev)
+        self._new_ids = torch.empty(self.batch, dtype=torch.int64, device=dev)
+        self.dispatched = torch.empty(self.batch, dtype=torch.int64, device=dev)
+
+    def decide(self, queries: torch.Tensor, prompt_len: torch.Tensor):
+        """Admit `batch` new requests, re-rank the queue, dispatch `batch`.
+
+        Returns the predict outputs of the new requests and the request ids
+        dispatched (arrival numbers, the first standing request being 0)."""
+        if queries.shape[0] != self.batch or prompt_len.shape[0] != self.batch:
+            raise SageError(f"a decision admits exactly {self.batch} requests")
+        pred = self.store.predict(queries, out=self._pred)
+        self.mass.index_copy_(0, self.free, pred[3])
+        self.prompt_len.index_copy_(0, self.free, prompt_len)
+        torch.add(self._arange, self.next_request, out=self._new_ids)
+        self.request.index_copy_(0, self.free, self._new_ids)
+        self.next_request += self.batch
+        index(self.mass, self.prompt_len, self.store.bin_repr, out=self.index)
+        rank(self.index, workspace=self._rank_ws, out=self.order)
+        self.free.copy_(self.order[:self.batch])
+        torch.index_select(self.request, 0, self.free, out=self.dispatched)
+        return pred, self.dispatched
+
+
 class StageTimer:
     """Per-kernel HIP-event timing of everything the library launches while attached."""
 

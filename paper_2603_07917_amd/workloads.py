@@ -37,7 +37,7 @@ import numpy as np
 SEED_BASE = 260307917
 # Order in which child streams are spawned; never reorder (changes every input).
 STREAMS = ("centres", "cluster_params", "assignment", "noise", "lengths",
-           "queries", "prompt_lengths", "masses")
+           "queries", "prompt_lengths", "masses", "standing")
 
 
 def streams(config_id: int, seed_base: int = SEED_BASE) -> dict:
@@ -243,6 +243,25 @@ def make_index(spec: IndexSpec, config_id: int, seed_base: int = SEED_BASE,
     prompt_len = _prompt_lengths(r["prompt_lengths"], spec.prompt, spec.Q)
     edges, repr_ = log_bins(spec.L_max, spec.B)
     return IndexInputs(spec, mass, prompt_len, edges, repr_, [seed_base, config_id])
+
+
+def make_standing(spec: PredictSpec, config_id: int, n: int, seed_base: int = SEED_BASE):
+    """The streaming workload's standing queue: n more requests from the same
+    mixture (embeddings and prompt lengths), drawn from the "standing" stream.
+    Returns (queries [n, d] float32, prompt_len [n] int32)."""
+    r = streams(config_id, seed_base)
+    centres = _unit_rows(r["centres"].standard_normal((spec.clusters, spec.d)))
+    cp = r["cluster_params"]
+    cp.uniform(*spec.mu_range, size=spec.clusters)      # same draws as make_predict
+    cp.uniform(*spec.s_range, size=spec.clusters)
+    probs = _cluster_probs(spec, cp)
+    rs = r["standing"]
+    q_cluster = rs.choice(spec.clusters, size=n, p=probs).astype(np.int32)
+    q_noise = rs.random(n) < spec.noise_frac
+    q_cluster = np.where(q_noise, -1, q_cluster).astype(np.int32)
+    queries = _points(rs, centres, q_cluster, spec, q_noise)
+    prompt_len = _prompt_lengths(rs, spec.prompt, n)
+    return queries, prompt_len
 
 
 def make_config(config_id: int, **overrides):
