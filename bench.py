@@ -33,8 +33,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 5],
-                    help="workload: 1 tiny, 2 mid (default), 3 gemm-bound, 5 streaming")
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                    help="workload: 1 tiny, 2 mid (default), 3 gemm-bound, 4 index-bound, 5 streaming")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -110,6 +110,8 @@ def main():
     torch.cuda.set_device(0)
     if args.config == 5:
         return run_streaming(args, torch, sage, workloads)
+    if args.config == 4:
+        return run_index_bound(args, torch, sage, workloads)
     w = workloads.make_config(args.config)
     spec = w.spec
     Q, N, d, k, B = spec.Q, spec.N, spec.d, spec.k, spec.B
@@ -205,6 +207,62 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def run_index_bound(args, torch, sage, workloads):
+    """The index-bound workload: 65,536 requests that already carry a
+    1,024-bin length distribution; a step is cost + Gittins index + rank."""
+    w = workloads.make_config(4)
+    spec = w.spec
+    Q, B = spec.Q, spec.B
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    mass, plen, repr_ = dev(w.mass), dev(w.prompt_len), dev(w.bin_repr)
+    g = torch.empty(Q, dtype=torch.float32, device="cuda")
+    order = torch.empty(Q, dtype=torch.int32, device="cuda")
+    rws = torch.empty(max(16, sage.rank_workspace_bytes(Q)), dtype=torch.uint8, device="cuda")
+
+    def step():
+        sage.index(mass, plen, repr_, out=g)
+        sage.rank(g, workspace=rws, out=order)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    timer = sage.StageTimer(capacity=64 * (args.steps + 1))
+    with timer:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    stages = timer.totals()
+    timer.close()
+    n_launch, k_ms = stages["index_scan"]
+    avg_s = k_ms / n_launch / 1e3
+    k_bytes = Q * (4.0 * B + 8.0)               # masses + prompt lengths in, index out
+    achieved = k_bytes / avg_s / 1e9
+    line = {
+        "metric": "scheduling decisions/sec (cost+index+rank)",
+        "value": Q * args.steps / elapsed,
+        "unit": "decisions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": workloads.WORKLOAD_NAMES[4], "Q": Q, "B": B, "alpha": spec.alpha,
+                   "seed": w.seed},
+        "roofline": {"bound": "hbm", "kernel": "index_kernel", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "avg_launch_us": avg_s * 1e6, "bytes_per_launch": k_bytes},
+        "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
+    }
     print(json.dumps(line), flush=True)
 
 

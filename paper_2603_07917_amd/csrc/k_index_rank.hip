@@ -13,120 +13,129 @@ namespace {
 // Candidates are compared by cross-multiplication (N_b F* < N* F_b), so a row
 // costs one fp64 division. All sums are fp64.
 // ---------------------------------------------------------------------------
-template <int C>
-__global__ void __launch_bounds__(256) index_kernel(const float* __restrict__ mass,
+template <int C, bool kFull>
+__device__ __forceinline__ void load_row(const float* __restrict__ mass, size_t row, int b0, int B,
+                                         float (&p)[C]) {
+  if (kFull && C % 4 == 0) {
+#pragma unroll
+    for (int j = 0; j < C; j += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(mass + row + b0 + j);
+      p[j] = v.x; p[j + 1] = v.y; p[j + 2] = v.z; p[j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < C; ++j) p[j] = (kFull || b0 + j < B) ? mass[row + b0 + j] : 0.0f;
+  }
+}
+
+// kFull: B == 64 C, so every lane owns C real bins (no guards, vector loads).
+// kFused: the support comes from the prompt length and the representatives
+// (kept in LDS), else from the given cost matrix.
+// Workgroups per CU the register budget is tuned for (4 waves each).
+template <int C> struct IndexOcc { static constexpr int value = C <= 8 ? 4 : (C == 16 ? 3 : 1); };
+
+template <int C, bool kFull, bool kFused>
+__global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const float* __restrict__ mass,
                                                     const float* __restrict__ cost,
                                                     const int32_t* __restrict__ prompt_len,
                                                     const double* __restrict__ repr, int Q, int B,
                                                     float* __restrict__ index,
                                                     int32_t* __restrict__ argmin) {
-  constexpr bool kCacheRepr = C <= 16;
+  extern __shared__ double repr_s[];               // [B] representatives (fused cost only)
   const int lane = (int)lane_id();
   const int wave = (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave);
   const int n_waves = (int)(gridDim.x * (blockDim.x / kWave));
   const int b0 = lane * C;
-  const bool fused = cost == nullptr;
-  const bool full = b0 + C <= B;
-  const bool vec = full && (C % 4 == 0) && (B % 4 == 0);
-
-  double r_c[kCacheRepr ? C : 1], h_c[kCacheRepr ? C : 1];
-  if (kCacheRepr && fused) {
-#pragma unroll
-    for (int j = 0; j < C; ++j) {
-      const int b = b0 + j;
-      const double r = b < B ? repr[b] : 0.0;
-      r_c[j] = r;
-      h_c[j] = r * r * 0.5;
-    }
+  if (kFused) {
+    for (int b = threadIdx.x; b < B; b += blockDim.x) repr_s[b] = repr[b];
+    __syncthreads();
   }
 
+  float p[C], p_next[C];
+  if (wave < Q) load_row<C, kFull>(mass, (size_t)wave * B, b0, B, p_next);
   for (int q = wave; q < Q; q += n_waves) {
     const size_t row = (size_t)q * (size_t)B;
-    float p[C];
-    if (vec) {
 #pragma unroll
-      for (int j = 0; j < C; j += 4) {
-        const float4 v = *reinterpret_cast<const float4*>(mass + row + b0 + j);
-        p[j] = v.x; p[j + 1] = v.y; p[j + 2] = v.z; p[j + 3] = v.w;
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < C; ++j) p[j] = (b0 + j < B) ? mass[row + b0 + j] : 0.0f;
-    }
-    const double I = fused ? (double)prompt_len[q] : 0.0;
+    for (int j = 0; j < C; ++j) p[j] = p_next[j];
+    if (q + n_waves < Q) load_row<C, kFull>(mass, row + (size_t)n_waves * B, b0, B, p_next);   // prefetch
+    const double I = kFused ? (double)prompt_len[q] : 0.0;
 
-    // Lane-local suffix masses and totals.
-    double t_loc[C];
-    double lane_f = 0.0;
+    // Support x_j = r (I + r / 2) (or the given cost); recomputed where used,
+    // which keeps the register count (and so the occupancy) down.
+    auto support = [&](int j) -> double {
+      const int b = b0 + j;
+      const bool in = kFull || b < B;
+      if (kFused) {
+        const double r = in ? repr_s[b] : 0.0;
+        return r * fma(0.5, r, I);
+      }
+      return in ? (double)cost[row + b] : 0.0;
+    };
+    double lane_f = 0.0, lane_s = 0.0;
 #pragma unroll
-    for (int j = C - 1; j >= 0; --j) {
-      t_loc[j] = lane_f;
+    for (int j = 0; j < C; ++j) {
       lane_f += (double)p[j];
+      lane_s = fma((double)p[j], support(j), lane_s);
     }
-    double lane_s = 0.0;
-    double x[C];
-#pragma unroll
-    for (int j = 0; j < C; ++j) {
-      const int b = b0 + j;
-      double xv;
-      if (fused) {
-        if (kCacheRepr) {
-          xv = fma(I, r_c[j], h_c[j]);
-        } else {
-          const double r = b < B ? repr[b] : 0.0;
-          xv = fma(I, r, r * r * 0.5);
-        }
-      } else {
-        xv = b < B ? (double)cost[row + b] : 0.0;
-      }
-      x[j] = xv;
-      lane_s = fma((double)p[j], xv, lane_s);
-    }
-    const double f_base = wave_excl_scan_f64(lane_f);
-    const double s_base = wave_excl_scan_f64(lane_s);
-    const double t_base = wave_excl_suffix_f64(lane_f);
+    // Prefix sums over lanes (DPP); the mass above this lane is the row total
+    // minus the inclusive prefix (fp64, so its rounding is ~1e-16 of the total).
+    const double f_incl = wave_incl_scan_dpp_f64(lane_f);
+    const double f_base = wave_shift_up_dpp_f64(f_incl);
+    const double s_base = wave_shift_up_dpp_f64(wave_incl_scan_dpp_f64(lane_s));
+    const double f_total = __longlong_as_double(
+        ((long long)__builtin_amdgcn_readlane((int)((uint64_t)__double_as_longlong(f_incl) >> 32), kWave - 1) << 32) |
+        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)__double_as_longlong(f_incl), kWave - 1));
+    const double t_base = f_total - f_incl;
 
-    double best_n = 0.0, best_f = 0.0;
+    // Branch-free running minimum of n / f by cross-multiplication; the
+    // start values (n, f) = (1, 0) lose to the first bin with f > 0, and a
+    // later bin must be strictly smaller to win (ties keep the lower bin).
+    double best_n = 1.0, best_f = 0.0;
     int best_b = -1;
-    double f_run = f_base, s_run = s_base;
+    double f_run = f_base, s_run = s_base, t_run = f_total - f_base;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
-      f_run += (double)p[j];
-      s_run = fma((double)p[j], x[j], s_run);
-      const int b = b0 + j;
-      if (f_run > 0.0 && b < B) {
-        const double n = fma(t_base + t_loc[j], x[j], s_run);
-        if (best_b < 0 || n * best_f < best_n * f_run) {
-          best_n = n; best_f = f_run; best_b = b;
-        }
-      }
+      const double pj = (double)p[j];
+      const double xj = support(j);
+      f_run += pj;
+      s_run = fma(pj, xj, s_run);
+      t_run -= pj;                                  // mass strictly above bin j
+      const double n = fma(t_run, xj, s_run);
+      const bool take = (kFull || b0 + j < B) && f_run > 0.0 && n * best_f < best_n * f_run;
+      best_n = take ? n : best_n;
+      best_f = take ? f_run : best_f;
+      best_b = take ? b0 + j : best_b;
     }
-    // Wave-wide minimum of n/f; ties keep the smaller bin.
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const double on = __shfl_xor(best_n, off, kWave);
-      const double of = __shfl_xor(best_f, off, kWave);
-      const int ob = __shfl_xor(best_b, off, kWave);
-      bool take = false;
-      if (ob >= 0) {
-        if (best_b < 0) {
-          take = true;
-        } else {
-          const double lhs = on * best_f, rhs = best_n * of;
-          take = lhs < rhs || (lhs == rhs && ob < best_b);
-        }
-      }
-      if (take) { best_n = on; best_f = of; best_b = ob; }
-    }
-    if (lane == 0) {
+    // Wave-wide minimum of n/f, ties keeping the smaller bin: butterflies
+    // within rows of 16 (quads, half rows, rows), then rows 0+1 -> 1, 2+3 -> 3
+    // and 1 -> 3; lane 63 ends with the row's result. The combine is
+    // idempotent, so lanes left out of a step simply combine with themselves.
+    auto combine = [&](double on, double of, int ob) {
+      const double lhs = on * best_f, rhs = best_n * of;
+      const bool take = ob >= 0 && (best_b < 0 || lhs < rhs || (lhs == rhs && ob < best_b));
+      best_n = take ? on : best_n;
+      best_f = take ? of : best_f;
+      best_b = take ? ob : best_b;
+    };
+#define SAGE_ARGMIN_STEP(CTRL, ROWS)                                                      \
+    combine(dpp_f64<CTRL, ROWS>(best_n, best_n), dpp_f64<CTRL, ROWS>(best_f, best_f),     \
+            (int)dpp_u32<CTRL, ROWS>((uint32_t)best_b, (uint32_t)best_b))
+    SAGE_ARGMIN_STEP(kDppQuadXor1, 0xf);
+    SAGE_ARGMIN_STEP(kDppQuadXor2, 0xf);
+    SAGE_ARGMIN_STEP(kDppRowHalfMirror, 0xf);
+    SAGE_ARGMIN_STEP(kDppRowMirror, 0xf);
+    SAGE_ARGMIN_STEP(kDppRowBcast15, 0xa);
+    SAGE_ARGMIN_STEP(kDppRowBcast31, 0xc);
+#undef SAGE_ARGMIN_STEP
+    if (lane == kWave - 1) {
       index[q] = best_b >= 0 ? (float)(best_n / best_f) : __builtin_inff();
       if (argmin) argmin[q] = best_b;
     }
   }
 }
 
-template <int C>
-hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* prompt_len,
+template <int C, bool kFull, bool kFused>
+hipError_t launch_index_v(const float* mass, const float* cost, const int32_t* prompt_len,
                           const double* repr, int Q, int B, float* index, int32_t* argmin,
                           hipStream_t stream) {
   const int waves_per_block = 4;
@@ -135,9 +144,21 @@ hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* p
   long blocks = (waves + waves_per_block - 1) / waves_per_block;
   if (blocks > 65535) blocks = 65535;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(index_kernel<C>, dim3((unsigned)blocks), dim3(64 * waves_per_block), 0, stream,
-                     mass, cost, prompt_len, repr, Q, B, index, argmin);
+  const size_t lds = kFused ? (size_t)B * sizeof(double) : 0;
+  hipLaunchKernelGGL((index_kernel<C, kFull, kFused>), dim3((unsigned)blocks), dim3(64 * waves_per_block),
+                     lds, stream, mass, cost, prompt_len, repr, Q, B, index, argmin);
   return hipGetLastError();
+}
+
+template <int C>
+hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* prompt_len,
+                          const double* repr, int Q, int B, float* index, int32_t* argmin,
+                          hipStream_t stream) {
+  const bool full = B == 64 * C, fused = cost == nullptr;
+  if (full && fused) return launch_index_v<C, true, true>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
+  if (full) return launch_index_v<C, true, false>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
+  if (fused) return launch_index_v<C, false, true>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
+  return launch_index_v<C, false, false>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
 }
 
 // ---------------------------------------------------------------------------

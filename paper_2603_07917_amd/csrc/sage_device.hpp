@@ -113,6 +113,41 @@ __device__ __forceinline__ double wave_excl_suffix_f64(double x) {
   return v;
 }
 
+// ---------------------------------------------------------------------------
+// DPP cross-lane moves (gfx9 wave64 encodings): no LDS round trip.
+// ---------------------------------------------------------------------------
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppWaveShr1 = 0x138, kDppRowMirror = 0x140, kDppRowHalfMirror = 0x141;
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E;     // quad_perm [1,0,3,2], [2,3,0,1]
+
+// Lanes whose source is outside the pattern, or whose row is not in
+// kRowMask, receive `old`.
+template <int kCtrl, int kRowMask = 0xf>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, kCtrl, kRowMask, 0xf, false);
+}
+template <int kCtrl, int kRowMask = 0xf>
+__device__ __forceinline__ double dpp_f64(double old, double x) {
+  const uint64_t o = (uint64_t)__double_as_longlong(old), v = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = dpp_u32<kCtrl, kRowMask>((uint32_t)o, (uint32_t)v);
+  const uint32_t hi = dpp_u32<kCtrl, kRowMask>((uint32_t)(o >> 32), (uint32_t)(v >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Inclusive prefix sum over the 64 lanes (rows of 16 first, then across rows).
+__device__ __forceinline__ double wave_incl_scan_dpp_f64(double x) {
+  x += dpp_f64<kDppRowShr1>(0.0, x);
+  x += dpp_f64<kDppRowShr2>(0.0, x);
+  x += dpp_f64<kDppRowShr4>(0.0, x);
+  x += dpp_f64<kDppRowShr8>(0.0, x);
+  x += dpp_f64<kDppRowBcast15, 0xa>(0.0, x);
+  x += dpp_f64<kDppRowBcast31, 0xc>(0.0, x);
+  return x;
+}
+// The inclusive value of the lane below (0 for lane 0): an exclusive prefix.
+__device__ __forceinline__ double wave_shift_up_dpp_f64(double x) { return dpp_f64<kDppWaveShr1>(0.0, x); }
+
 __device__ __forceinline__ int wave_sum_i32(int x) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
