@@ -205,6 +205,40 @@ def gittins(mass, x):
     return G, arg
 
 
+def attained_service(prompt_len, generated, bucket: int) -> np.ndarray:
+    """Service already received by a running request, at its last refresh.
+
+    Sec. 3.3 refreshes a running request's index only at bucket boundaries
+    (bucket size 200 by default, Sec. 4); reading: a boundary every `bucket`
+    generated tokens. The service is the cost model of Sec. 3.2 at the
+    boundary: o = bucket * floor(generated / bucket), a = o^2 / 2 + I * o.
+    """
+    if bucket < 1:
+        raise ValueError("attained_service: bucket must be >= 1")
+    I = np.asarray(prompt_len, dtype=np.float64)
+    o = np.floor(np.asarray(generated, dtype=np.float64) / bucket) * bucket
+    return o * o / 2.0 + I * o
+
+
+def gittins_attained(mass, x, a):
+    """Gittins index of the remaining cost of running requests (Sec. 3.3).
+
+    A request that has received service a is known to need X > a, and what
+    remains is Y = X - a. Its index is the Gittins index of Y:
+        inf over Delta > 0 of E[min(X - a, Delta); X > a] / P(a < X <= a + Delta),
+    i.e. ``gittins`` applied to the masses of the support points above a
+    (those at or below a are ruled out) shifted down by a. a = 0 gives the
+    index at arrival. A row with no mass above a gets +inf (argmin -1).
+    """
+    p = np.asarray(mass, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64)
+    if x.ndim == 1:
+        x = np.broadcast_to(x, p.shape)
+    a = np.asarray(a, dtype=np.float64).reshape(-1, 1)
+    alive = x > a
+    return gittins(np.where(alive, p, 0.0), np.where(alive, x - a, 0.0))
+
+
 # ------------------------------------------------------------------ rank
 def rank(G) -> np.ndarray:
     """Queue order: ascending index, ties to the lower request id."""

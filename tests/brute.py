@@ -118,3 +118,26 @@ def gittins_by_delta(p, x, extra_points=()):
 
 def stable_order(keys):
     return sorted(range(len(keys)), key=lambda i: (keys[i], i))
+
+
+def gittins_attained_by_delta(p, x, a, extra_points=()):
+    """inf over Delta > 0 of E[min(X - a, Delta); X > a] / P(a < X <= a + Delta).
+
+    Evaluated directly at Delta = (support point - a) for every support point
+    above a, at midpoints between those, just above the largest, and at any
+    ``extra_points``; Deltas with P(a < X <= a + Delta) = 0 are skipped.
+    Returns the minimum, or None when no mass lies above a.
+    """
+    above = sorted(set(xi - a for xi in x if xi > a))
+    deltas = list(above) + [(u + v) / 2 for u, v in zip(above, above[1:])]
+    if above:
+        deltas.append(above[-1] + 1)
+    deltas += [d for d in extra_points if d > 0]
+    best = None
+    for D in deltas:
+        spend = sum((pi * min(xi - a, D) for pi, xi in zip(p, x) if xi > a), Fraction(0))
+        done = sum((pi for pi, xi in zip(p, x) if a < xi <= a + D), Fraction(0))
+        if done > 0:
+            r = spend / done
+            best = r if best is None or r < best else best
+    return best
