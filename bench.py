@@ -243,6 +243,21 @@ def run_index_bound(args, torch, sage, workloads):
     avg_s = k_ms / n_launch / 1e3
     k_bytes = Q * (4.0 * B + 8.0)               # masses + prompt lengths in, index out
     achieved = k_bytes / avg_s / 1e9
+
+    # The refresh of running requests (attained service, bucket 200) on the same rows.
+    gen = dev(workloads.generated_tokens(4, Q, spec.L_max))
+    for _ in range(args.warmup):
+        sage.index_attained(mass, plen, repr_, gen, 200, out=g)
+    torch.cuda.synchronize()
+    timer = sage.StageTimer(capacity=64 * (args.steps + 1))
+    with timer:
+        for _ in range(args.steps):
+            sage.index_attained(mass, plen, repr_, gen, 200, out=g)
+        torch.cuda.synchronize()
+    n_att, att_ms = timer.totals()["index_attained"]
+    timer.close()
+    att_s = att_ms / n_att / 1e3
+    att_bytes = Q * (4.0 * B + 12.0)
     line = {
         "metric": "scheduling decisions/sec (cost+index+rank)",
         "value": Q * args.steps / elapsed,
@@ -262,6 +277,10 @@ def run_index_bound(args, torch, sage, workloads):
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None, "avg_launch_us": avg_s * 1e6, "bytes_per_launch": k_bytes},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
+        "attained_refresh": {"kernel": "index_kernel (attained)", "bucket": 200,
+                             "running_rows": int((gen > 0).sum().item()), "avg_launch_us": att_s * 1e6,
+                             "achieved_GBs": att_bytes / att_s / 1e9,
+                             "frac_of_hbm_peak": att_bytes / att_s / 1e9 / HBM_PEAK_GBS},
     }
     print(json.dumps(line), flush=True)
 

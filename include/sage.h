@@ -141,6 +141,27 @@ int sage_index(const float* mass, const float* cost, const int32_t* prompt_len,
                const double* bin_repr, int Q, int B,
                float* index, int32_t* argmin_bin, sage_stream_t stream);
 
+/*
+ * sage_index_attained - the index of running requests, refreshed with the
+ * service they have already received (Sec. 3.3: the index of each active
+ * request is updated with its remaining cost distribution, only at bucket
+ * boundaries; bucket size 200 by default, Sec. 4). For request q with
+ * generated[q] output tokens so far, o = bucket * floor(generated[q] / bucket)
+ * and the service received is a = o^2 / 2 + I_q o (the cost model of
+ * sage_cost). Support points x <= a are ruled out and the remaining cost is
+ * X - a, so
+ *   G = inf over Delta > 0 of E[min(X - a, Delta); X > a] / P(a < X <= a + Delta),
+ * the minimum over the support points above a. generated[q] = 0 gives
+ * sage_index's result; a row with no mass above a gets +inf (argmin -1).
+ *   mass [Q, B] f32, prompt_len [Q] int32, bin_repr [B] f64 (as sage_index
+ *        with the fused cost), generated [Q] int32 >= 0, bucket >= 1
+ *   index [Q] f32 out, argmin_bin [Q] int32 out or NULL
+ * Errors as sage_index; SAGE_EINVAL also for bucket < 1.
+ */
+int sage_index_attained(const float* mass, const int32_t* prompt_len, const double* bin_repr,
+                        const int32_t* generated, int bucket, int Q, int B,
+                        float* index, int32_t* argmin_bin, sage_stream_t stream);
+
 /* sage_rank_workspace_bytes - device workspace bytes for sage_rank(Q). */
 size_t sage_rank_workspace_bytes(int Q);
 

@@ -29,18 +29,25 @@ __device__ __forceinline__ void load_row(const float* __restrict__ mass, size_t 
 }
 
 // kFull: B == 64 C, so every lane owns C real bins (no guards, vector loads).
-// kFused: the support comes from the prompt length and the representatives
-// (kept in LDS), else from the given cost matrix.
+// kMode: kGivenCost takes the support from the cost matrix; kFused computes
+// it from the prompt length and the representatives (kept in LDS);
+// kAttained also refreshes running requests: with o = bucket *
+// floor(generated / bucket) tokens served, a = o^2 / 2 + I o, the bins with
+// x <= a are ruled out and the rest are shifted down by a, so the result is
+// the index of the remaining cost.
+enum IndexMode { kGivenCost = 0, kFused = 1, kAttained = 2 };
 // Workgroups per CU the register budget is tuned for (4 waves each).
 template <int C> struct IndexOcc { static constexpr int value = C <= 8 ? 4 : (C == 16 ? 3 : 1); };
 
-template <int C, bool kFull, bool kFused>
+template <int C, bool kFull, int kMode>
 __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const float* __restrict__ mass,
                                                     const float* __restrict__ cost,
                                                     const int32_t* __restrict__ prompt_len,
-                                                    const double* __restrict__ repr, int Q, int B,
-                                                    float* __restrict__ index,
+                                                    const double* __restrict__ repr,
+                                                    const int32_t* __restrict__ generated, int bucket,
+                                                    int Q, int B, float* __restrict__ index,
                                                     int32_t* __restrict__ argmin) {
+  constexpr bool kFused = kMode != kGivenCost;
   extern __shared__ double repr_s[];               // [B] representatives (fused cost only)
   const int lane = (int)lane_id();
   const int wave = (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave);
@@ -59,6 +66,11 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     for (int j = 0; j < C; ++j) p[j] = p_next[j];
     if (q + n_waves < Q) load_row<C, kFull>(mass, row + (size_t)n_waves * B, b0, B, p_next);   // prefetch
     const double I = kFused ? (double)prompt_len[q] : 0.0;
+    double a = 0.0;                                 // service already received
+    if (kMode == kAttained) {
+      const double o = (double)((max(generated[q], 0) / bucket) * bucket);
+      a = o * fma(0.5, o, I);
+    }
 
     // Support x_j = r (I + r / 2) (or the given cost); recomputed where used,
     // which keeps the register count (and so the occupancy) down.
@@ -71,11 +83,15 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
       }
       return in ? (double)cost[row + b] : 0.0;
     };
+    if (kMode == kAttained) {                       // rule out the outcomes already passed
+#pragma unroll
+      for (int j = 0; j < C; ++j) p[j] = support(j) > a ? p[j] : 0.0f;
+    }
     double lane_f = 0.0, lane_s = 0.0;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
       lane_f += (double)p[j];
-      lane_s = fma((double)p[j], support(j), lane_s);
+      lane_s = fma((double)p[j], support(j) - a, lane_s);
     }
     // Prefix sums over lanes (DPP); the mass above this lane is the row total
     // minus the inclusive prefix (fp64, so its rounding is ~1e-16 of the total).
@@ -96,7 +112,7 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
 #pragma unroll
     for (int j = 0; j < C; ++j) {
       const double pj = (double)p[j];
-      const double xj = support(j);
+      const double xj = support(j) - a;
       f_run += pj;
       s_run = fma(pj, xj, s_run);
       t_run -= pj;                                  // mass strictly above bin j
@@ -134,31 +150,40 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
   }
 }
 
-template <int C, bool kFull, bool kFused>
+template <int C, bool kFull, int kMode>
 hipError_t launch_index_v(const float* mass, const float* cost, const int32_t* prompt_len,
-                          const double* repr, int Q, int B, float* index, int32_t* argmin,
-                          hipStream_t stream) {
+                          const double* repr, const int32_t* generated, int bucket, int Q, int B,
+                          float* index, int32_t* argmin, hipStream_t stream) {
   const int waves_per_block = 4;
   const int rows_per_wave = 4;
   long waves = ((long)Q + rows_per_wave - 1) / rows_per_wave;
   long blocks = (waves + waves_per_block - 1) / waves_per_block;
   if (blocks > 65535) blocks = 65535;
   if (blocks < 1) blocks = 1;
-  const size_t lds = kFused ? (size_t)B * sizeof(double) : 0;
-  hipLaunchKernelGGL((index_kernel<C, kFull, kFused>), dim3((unsigned)blocks), dim3(64 * waves_per_block),
-                     lds, stream, mass, cost, prompt_len, repr, Q, B, index, argmin);
+  const size_t lds = kMode != kGivenCost ? (size_t)B * sizeof(double) : 0;
+  hipLaunchKernelGGL((index_kernel<C, kFull, kMode>), dim3((unsigned)blocks), dim3(64 * waves_per_block),
+                     lds, stream, mass, cost, prompt_len, repr, generated, bucket, Q, B, index, argmin);
   return hipGetLastError();
 }
 
 template <int C>
 hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* prompt_len,
-                          const double* repr, int Q, int B, float* index, int32_t* argmin,
-                          hipStream_t stream) {
-  const bool full = B == 64 * C, fused = cost == nullptr;
-  if (full && fused) return launch_index_v<C, true, true>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
-  if (full) return launch_index_v<C, true, false>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
-  if (fused) return launch_index_v<C, false, true>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
-  return launch_index_v<C, false, false>(mass, cost, prompt_len, repr, Q, B, index, argmin, stream);
+                          const double* repr, const int32_t* generated, int bucket, int Q, int B,
+                          float* index, int32_t* argmin, hipStream_t stream) {
+  const bool full = B == 64 * C;
+  const int mode = generated ? kAttained : (cost ? kGivenCost : kFused);
+#define SAGE_INDEX_LAUNCH(FULL, MODE)                                                               \
+  return launch_index_v<C, FULL, MODE>(mass, cost, prompt_len, repr, generated, bucket, Q, B, index, \
+                                       argmin, stream)
+  if (full) {
+    if (mode == kAttained) SAGE_INDEX_LAUNCH(true, kAttained);
+    if (mode == kFused) SAGE_INDEX_LAUNCH(true, kFused);
+    SAGE_INDEX_LAUNCH(true, kGivenCost);
+  }
+  if (mode == kAttained) SAGE_INDEX_LAUNCH(false, kAttained);
+  if (mode == kFused) SAGE_INDEX_LAUNCH(false, kFused);
+  SAGE_INDEX_LAUNCH(false, kGivenCost);
+#undef SAGE_INDEX_LAUNCH
 }
 
 // ---------------------------------------------------------------------------
@@ -405,18 +430,21 @@ size_t rank_workspace_bytes(int Q) {
 }
 
 hipError_t launch_index(const float* mass, const float* cost, const int32_t* prompt_len,
-                        const double* bin_repr, int Q, int B, float* index, int32_t* argmin,
-                        hipStream_t stream) {
+                        const double* bin_repr, const int32_t* generated, int bucket, int Q, int B,
+                        float* index, int32_t* argmin, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
-  LaunchScope scope("index_scan", stream);
+  LaunchScope scope(generated ? "index_attained" : "index_scan", stream);
   const int per_lane = (B + kWave - 1) / kWave;
-  if (per_lane <= 1) return launch_index_c<1>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
-  if (per_lane <= 2) return launch_index_c<2>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
-  if (per_lane <= 4) return launch_index_c<4>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
-  if (per_lane <= 8) return launch_index_c<8>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
-  if (per_lane <= 16) return launch_index_c<16>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
-  if (per_lane <= 32) return launch_index_c<32>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
-  return launch_index_c<64>(mass, cost, prompt_len, bin_repr, Q, B, index, argmin, stream);
+#define SAGE_INDEX_C(CC) \
+  return launch_index_c<CC>(mass, cost, prompt_len, bin_repr, generated, bucket, Q, B, index, argmin, stream)
+  if (per_lane <= 1) SAGE_INDEX_C(1);
+  if (per_lane <= 2) SAGE_INDEX_C(2);
+  if (per_lane <= 4) SAGE_INDEX_C(4);
+  if (per_lane <= 8) SAGE_INDEX_C(8);
+  if (per_lane <= 16) SAGE_INDEX_C(16);
+  if (per_lane <= 32) SAGE_INDEX_C(32);
+  SAGE_INDEX_C(64);
+#undef SAGE_INDEX_C
 }
 
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream) {

@@ -311,8 +311,27 @@ SAGE_API int sage_index(const float* mass, const float* cost, const int32_t* pro
     if (p && !aligned16(p)) return fail(SAGE_EINVAL, "sage_index: misaligned pointer");
   int st = check_device();
   if (st != SAGE_OK) return st;
-  return hip_status(sage::launch_index(mass, cost, prompt_len, bin_repr, Q, B, index, argmin_bin,
+  return hip_status(sage::launch_index(mass, cost, prompt_len, bin_repr, nullptr, 1, Q, B, index, argmin_bin,
                                        (hipStream_t)stream),
+                    "index launch");
+}
+
+SAGE_API int sage_index_attained(const float* mass, const int32_t* prompt_len, const double* bin_repr,
+                                 const int32_t* generated, int bucket, int Q, int B, float* index,
+                                 int32_t* argmin_bin, sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (bucket < 1) return fail(SAGE_EINVAL, "bucket=%d must be >= 1", bucket);
+  if (Q == 0) return ok();
+  if (!mass || !prompt_len || !bin_repr || !generated || !index)
+    return fail(SAGE_EINVAL, "sage_index_attained: NULL required pointer");
+  const void* ptrs[] = {mass, prompt_len, bin_repr, generated, index, argmin_bin};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(SAGE_EINVAL, "sage_index_attained: misaligned pointer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_index(mass, nullptr, prompt_len, bin_repr, generated, bucket, Q, B, index,
+                                       argmin_bin, (hipStream_t)stream),
                     "index launch");
 }
 

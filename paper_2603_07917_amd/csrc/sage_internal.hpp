@@ -48,8 +48,8 @@ hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStre
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
                        float* cost, hipStream_t stream);
 hipError_t launch_index(const float* mass, const float* cost, const int32_t* prompt_len,
-                        const double* bin_repr, int Q, int B, float* index, int32_t* argmin,
-                        hipStream_t stream);
+                        const double* bin_repr, const int32_t* generated, int bucket, int Q, int B,
+                        float* index, int32_t* argmin, hipStream_t stream);
 size_t rank_workspace_bytes(int Q);
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream);
 // Neighbours of every query: ids [Q, k] and sims [Q, k] (sorted, padded).

@@ -41,6 +41,7 @@ def load_library():
         "sage_histogram": (I, [P, P, I, I, P, I, F, P, I, P, P, S]),
         "sage_cost": (I, [P, I, P, I, P, S]),
         "sage_index": (I, [P, P, P, P, I, I, P, P, S]),
+        "sage_index_attained": (I, [P, P, P, P, I, I, I, P, P, S]),
         "sage_rank_workspace_bytes": (Z, [I]),
         "sage_rank": (I, [P, I, P, P, Z, S]),
         "sage_status_string": (ctypes.c_char_p, [I]),
@@ -174,6 +175,25 @@ def index(mass: torch.Tensor, prompt_len: Optional[torch.Tensor] = None,
     arg = torch.empty(Q, dtype=torch.int32, device=mass.device) if with_argmin else None
     _check(load_library().sage_index(_ptr(mass), _ptr(cost), _ptr(prompt_len), _ptr(bin_repr), Q, B,
                                      _ptr(g), _ptr(arg), _stream()))
+    return (g, arg) if with_argmin else g
+
+
+def index_attained(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor,
+                   generated: torch.Tensor, bucket: int = 200, with_argmin: bool = False,
+                   out: Optional[torch.Tensor] = None):
+    """Index of running requests from their remaining cost (refreshed at bucket boundaries)."""
+    _dev(mass, torch.float32, "mass", 2)
+    _dev(prompt_len, torch.int32, "prompt_len", 1)
+    _dev(bin_repr, torch.float64, "bin_repr", 1)
+    _dev(generated, torch.int32, "generated", 1)
+    Q, B = mass.shape
+    if prompt_len.shape[0] != Q or generated.shape[0] != Q or bin_repr.shape[0] != B:
+        raise SageError("prompt_len / generated / bin_repr do not match mass")
+    g = out if out is not None else torch.empty(Q, dtype=torch.float32, device=mass.device)
+    arg = torch.empty(Q, dtype=torch.int32, device=mass.device) if with_argmin else None
+    _check(load_library().sage_index_attained(_ptr(mass), _ptr(prompt_len), _ptr(bin_repr),
+                                              _ptr(generated), int(bucket), Q, B, _ptr(g), _ptr(arg),
+                                              _stream()))
     return (g, arg) if with_argmin else g
 
 

@@ -37,7 +37,7 @@ import numpy as np
 SEED_BASE = 260307917
 # Order in which child streams are spawned; never reorder (changes every input).
 STREAMS = ("centres", "cluster_params", "assignment", "noise", "lengths",
-           "queries", "prompt_lengths", "masses", "standing")
+           "queries", "prompt_lengths", "masses", "standing", "attained")
 
 
 def streams(config_id: int, seed_base: int = SEED_BASE) -> dict:
@@ -262,6 +262,17 @@ def make_standing(spec: PredictSpec, config_id: int, n: int, seed_base: int = SE
     queries = _points(rs, centres, q_cluster, spec, q_noise)
     prompt_len = _prompt_lengths(rs, spec.prompt, n)
     return queries, prompt_len
+
+
+def generated_tokens(config_id: int, Q: int, L_max: int, running: float = 0.5,
+                     seed_base: int = SEED_BASE) -> np.ndarray:
+    """Output tokens already generated by each request (0 for those not yet
+    started): a fraction `running` of the requests are running, with
+    floor(L_max * u^2 / 4), u ~ U(0, 1), tokens so far. int32 [Q]."""
+    r = streams(config_id, seed_base)["attained"]
+    run = r.random(Q) < running
+    u = r.random(Q)
+    return np.where(run, np.floor(L_max * u * u / 4.0), 0).astype(np.int32)
 
 
 def make_config(config_id: int, **overrides):

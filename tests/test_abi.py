@@ -33,6 +33,7 @@ def lib():
     lib.sage_rank_workspace_bytes.argtypes = [I]
     lib.sage_rank_workspace_bytes.restype = Z
     lib.sage_index.argtypes = [P, P, P, P, I, I, P, P, P]
+    lib.sage_index_attained.argtypes = [P, P, P, P, I, I, I, P, P, P]
     lib.sage_rank.argtypes = [P, I, P, P, Z, P]
     lib.sage_cost.argtypes = [P, I, P, I, P, P]
     lib.sage_histogram.argtypes = [P, P, I, I, P, I, F, P, I, P, P, P]
@@ -116,6 +117,12 @@ def test_index_rank_cost_hist_validation(lib):
     assert lib.sage_index(None, A, None, None, 4, 16, A, None, None) == SAGE_EINVAL
     assert lib.sage_index(A + 8, A, None, None, 4, 16, A, None, None) == SAGE_EINVAL
     assert lib.sage_index(None, None, None, None, 0, 16, None, None, None) == SAGE_OK
+    # sage_index_attained(mass, prompt_len, bin_repr, generated, bucket, Q, B, index, argmin, stream)
+    assert lib.sage_index_attained(A, A, A, A, 0, 4, 16, A, None, None) == SAGE_EINVAL      # bucket < 1
+    assert lib.sage_index_attained(A, A, A, None, 200, 4, 16, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index_attained(A, A, A, A + 4, 200, 4, 16, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index_attained(A, A, A, A, 200, 4, 5000, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index_attained(None, None, None, None, 200, 0, 16, None, None, None) == SAGE_OK
     assert lib.sage_rank(A, 10, A, A, 0, None) == SAGE_EWORKSPACE
     assert lib.sage_rank(None, 10, A, A, 1 << 20, None) == SAGE_EINVAL
     assert lib.sage_rank(A, -1, A, A, 1 << 20, None) == SAGE_EINVAL

@@ -134,3 +134,48 @@ def test_histogram_vs_oracle(k, B, tau):
     sims[10:20] = rng.uniform(0.1, 0.5, size=(10, k)).astype(np.float32)   # all below tau
     counts, mass = sage.histogram(dev(ids), dev(sims), dev(L), tau, dev(edges))
     parity.check_hist(ids, sims, host(counts), host(mass), L, edges, tau)
+
+
+# ------------------------------------------------------- index refresh (attained service)
+def test_index_attained_vs_oracle_full_index_workload():
+    w = workloads.make_config(4)
+    spec = w.spec
+    gen = workloads.generated_tokens(4, spec.Q, spec.L_max)
+    g = host(sage.index_attained(dev(w.mass), dev(w.prompt_len), dev(w.bin_repr), dev(gen), 200))
+    a = oracle.attained_service(w.prompt_len, gen, 200)
+    G, _ = oracle.gittins_attained(w.mass.astype(np.float64), oracle.cost(w.prompt_len, w.bin_repr), a)
+    inf = np.isinf(G)
+    assert np.array_equal(np.isinf(g), inf)
+    rel = np.abs(g[~inf].astype(np.float64) - G[~inf]) / np.abs(G[~inf])
+    assert rel.max(initial=0.0) <= parity.INDEX_RTOL, rel.max()
+    assert (gen > 0).sum() > spec.Q // 3                             # many running rows
+    print(f"attained: {int((gen > 0).sum())} running rows, {int(inf.sum())} with no mass left")
+
+
+@pytest.mark.parametrize("B", [7, 64, 256, 1024])
+def test_index_attained_zero_is_the_index_and_argmin(B):
+    rng = np.random.default_rng(B)
+    Q = 300
+    mass = rng.dirichlet(np.full(B, 0.3), size=Q).astype(np.float32)
+    plen = rng.integers(8, 4000, size=Q).astype(np.int32)
+    edges, r = workloads.log_bins(16384, B)
+    g0 = host(sage.index(dev(mass), dev(plen), dev(r)))
+    ga = host(sage.index_attained(dev(mass), dev(plen), dev(r), dev(np.zeros(Q, np.int32)), 200))
+    assert np.array_equal(g0.view(np.uint32), ga.view(np.uint32))
+    gen = rng.integers(0, 3000, size=Q).astype(np.int32)
+    gen[:5] = 20000                                               # past every support point (L_max 16384)
+    for bucket in (1, 200):
+        g, arg = sage.index_attained(dev(mass), dev(plen), dev(r), dev(gen), bucket, with_argmin=True)
+        g, arg = host(g), host(arg)
+        x = oracle.cost(plen, r)
+        G, A = oracle.gittins_attained(mass.astype(np.float64), x, oracle.attained_service(plen, gen, bucket))
+        inf = np.isinf(G)
+        assert np.array_equal(np.isinf(g), inf) and np.all(arg[inf] == -1)
+        rel = np.abs(g[~inf].astype(np.float64) - G[~inf]) / G[~inf]
+        assert rel.max(initial=0.0) <= parity.INDEX_RTOL
+        assert np.all(inf[:5])
+        # the argmin attains the minimum (within the tolerance) and lies above the served cost
+        a = oracle.attained_service(plen, gen, bucket)
+        ok = ~inf
+        rows = np.nonzero(ok)[0]
+        assert np.all(x[rows, arg[rows]] > a[rows])
