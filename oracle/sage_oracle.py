@@ -132,14 +132,18 @@ def bin_of(lengths, edges) -> np.ndarray:
     return np.clip(b, 0, B - 1).astype(np.int64)
 
 
-def histogram(ids, sims, hist_len, edges, tau: float):
+def histogram(ids, sims, hist_len, edges, tau: float, weighting: str = "similarity"):
     """Per-request output-length distribution from its neighbours.
 
     counts[q, b]: neighbours (valid ids only) whose length falls in bin b.
     mass[q, b]  : sum of w_i over those neighbours / sum of all w_i, where
                   w_i = s_i if s_i >= tau else 0; if every w_i is 0 the mass
                   falls back to counts / (number of valid neighbours).
+    weighting="uniform" is the paper's own form (Sec. 3.1): every neighbour
+    at or above the threshold counts once, w_i = 1 if s_i >= tau else 0.
     """
+    if weighting not in ("similarity", "uniform"):
+        raise ValueError(f"histogram: unknown weighting {weighting!r}")
     ids = np.asarray(ids)
     sims = np.asarray(sims, dtype=np.float64)
     Q, _ = ids.shape
@@ -154,7 +158,7 @@ def histogram(ids, sims, hist_len, edges, tau: float):
             continue
         b = bin_of(hist_len[ids[q][valid]], edges)
         s = sims[q][valid]
-        w = np.where(s >= tau, s, 0.0)
+        w = np.where(s >= tau, s if weighting == "similarity" else 1.0, 0.0)
         np.add.at(counts[q], b, 1)
         W = w.sum()
         if W > 0:
@@ -171,6 +175,47 @@ def cost(prompt_len, bin_repr) -> np.ndarray:
     I = np.asarray(prompt_len, dtype=np.float64)[:, None]
     r = np.asarray(bin_repr, dtype=np.float64)[None, :]
     return r * r / 2.0 + I * r
+
+
+def cost_variant(prompt_len, bin_repr, model: str) -> np.ndarray:
+    """The cost models the paper compares against (Sec. 4 ablation):
+    "resource" = O^2/2 + I O (the adopted one, ``cost``), "output" = O (the
+    output length alone), "overall" = I + 2 O (input and output lengths,
+    output weighted double), each at O = r_b."""
+    I = np.asarray(prompt_len, dtype=np.float64)[:, None]
+    r = np.asarray(bin_repr, dtype=np.float64)[None, :]
+    if model == "resource":
+        return cost(prompt_len, bin_repr)
+    if model == "output":
+        return np.broadcast_to(r, (I.shape[0], r.shape[1])).copy()
+    if model == "overall":
+        return I + 2.0 * r
+    raise ValueError(f"cost_variant: unknown model {model!r}")
+
+
+def mix_uniform(mass, weight: float) -> np.ndarray:
+    """A prediction made deliberately inaccurate (Sec. 4 ablation): a uniform
+    distribution over the bins merged with the row's distribution at
+    weight : (1 - weight), i.e. 1:4 for weight 0.2. Rows with no mass stay
+    empty."""
+    p = np.asarray(mass, dtype=np.float64)
+    B = p.shape[1]
+    tot = p.sum(axis=1, keepdims=True)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        mixed = (1.0 - weight) * p / tot + weight / B
+    return np.where(tot > 0, mixed, p)
+
+
+def mean_index(mass, x):
+    """The Mean baseline (Sec. 4 ablation): E[X] = sum p x / sum p; +inf for
+    a row with no mass."""
+    p = np.asarray(mass, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64)
+    if x.ndim == 1:
+        x = np.broadcast_to(x, p.shape)
+    tot = p.sum(axis=1)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return np.where(tot > 0, (p * x).sum(axis=1) / tot, np.inf)
 
 
 # ----------------------------------------------------------------- index

@@ -67,8 +67,9 @@ def bin_linear(L, edges):
     return best
 
 
-def histogram_exact(ids, sims, lengths, edges, tau):
-    """One request's counts and masses with Fractions (sims given as floats)."""
+def histogram_exact(ids, sims, lengths, edges, tau, uniform=False):
+    """One request's counts and masses with Fractions (sims given as floats);
+    uniform=True weighs every neighbour at or above tau by 1 instead of s."""
     B = len(edges) - 1
     counts = [0] * B
     wsum = [Fraction(0)] * B
@@ -78,7 +79,7 @@ def histogram_exact(ids, sims, lengths, edges, tau):
         b = bin_linear(lengths[i], edges)
         counts[b] += 1
         if s >= t:
-            wsum[b] += s
+            wsum[b] += 1 if uniform else s
     W = sum(wsum, Fraction(0))
     m = len(valid)
     if W > 0:
