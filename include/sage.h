@@ -162,6 +162,44 @@ int sage_index_attained(const float* mass, const int32_t* prompt_len, const doub
                         const int32_t* generated, int bucket, int Q, int B,
                         float* index, int32_t* argmin_bin, sage_stream_t stream);
 
+/*
+ * Variants of the method that the paper compares against (Sec. 4 ablation).
+ *
+ * sage_histogram_variant - sage_histogram with a choice of neighbour weight:
+ *   SAGE_WEIGHT_SIMILARITY: w = s if s >= tau (sage_histogram's form);
+ *   SAGE_WEIGHT_UNIFORM:    w = 1 if s >= tau, the paper's own form (Sec. 3.1:
+ *                           the outputs of the similar requests form the
+ *                           distribution, each counting once).
+ * Same arguments, fallback and errors as sage_histogram; SAGE_EINVAL for an
+ * unknown weighting.
+ */
+enum { SAGE_WEIGHT_SIMILARITY = 0, SAGE_WEIGHT_UNIFORM = 1 };
+int sage_histogram_variant(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
+                           const int32_t* hist_len, int N, float tau, const double* bin_edges, int B,
+                           int weighting, int32_t* counts, float* mass, sage_stream_t stream);
+
+/*
+ * sage_index_variant - a priority index under the paper's alternative
+ * choices, on the fused cost (support at O = bin_repr[b]):
+ *   cost_model SAGE_COST_RESOURCE: O^2/2 + I O (the adopted model, sage_cost)
+ *              SAGE_COST_OUTPUT:   O (output length alone)
+ *              SAGE_COST_OVERALL:  I + 2 O (input plus doubled output length)
+ *   index_kind SAGE_INDEX_GITTINS: as sage_index
+ *              SAGE_INDEX_MEAN:    E[X] = sum p x / sum p (the Mean baseline;
+ *                                  argmin_bin is -1)
+ *   noise_weight in [0, 1): the distribution is first mixed with the uniform
+ *              one, p' = (1 - w) p / sum(p) + w / B (w = 0.2 is the paper's
+ *              1:4 inaccurate prediction); rows with no mass stay empty.
+ * mass [Q, B] f32, prompt_len [Q] int32, bin_repr [B] f64; index [Q] f32 out
+ * (+inf for a row with no mass), argmin_bin [Q] int32 out or NULL.
+ * SAGE_EINVAL for unknown enums or noise_weight outside [0, 1).
+ */
+enum { SAGE_COST_RESOURCE = 0, SAGE_COST_OUTPUT = 1, SAGE_COST_OVERALL = 2 };
+enum { SAGE_INDEX_GITTINS = 0, SAGE_INDEX_MEAN = 1 };
+int sage_index_variant(const float* mass, const int32_t* prompt_len, const double* bin_repr, int Q, int B,
+                       int cost_model, int index_kind, float noise_weight,
+                       float* index, int32_t* argmin_bin, sage_stream_t stream);
+
 /* sage_rank_workspace_bytes - device workspace bytes for sage_rank(Q). */
 size_t sage_rank_workspace_bytes(int Q);
 

@@ -24,11 +24,13 @@ __device__ __forceinline__ int length_bin(const double* __restrict__ edges, int 
 
 // One wavefront per request; QPB requests per workgroup share nothing but
 // the launch. LDS per wave: B int32 counts + B uint64 fixed-point weights.
+// A neighbour at or above tau weighs its similarity, or 1 when `uniform`
+// (the paper's unweighted form).
 template <int QPB>
 __global__ void __launch_bounds__(64 * QPB) hist_kernel(
     const int32_t* __restrict__ ids, const float* __restrict__ sims, int Q, int k,
     const int32_t* __restrict__ hist_len, int N, float tau, const double* __restrict__ edges, int B,
-    int32_t* __restrict__ counts, float* __restrict__ mass) {
+    int uniform, int32_t* __restrict__ counts, float* __restrict__ mass) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int w = threadIdx.x / kWave;
   const int lane = (int)lane_id();
@@ -53,7 +55,7 @@ __global__ void __launch_bounds__(64 * QPB) hist_kernel(
       ++m;
       const float s = sims[row + i];
       if (s >= tau) {
-        const uint64_t fx = (uint64_t)((double)s * kWeightScale);
+        const uint64_t fx = (uint64_t)((uniform ? 1.0 : (double)s) * kWeightScale);
         atomicAdd(reinterpret_cast<unsigned long long*>(&wsum[b]), (unsigned long long)fx);
         wtot += fx;
       }
@@ -81,19 +83,19 @@ __global__ void __launch_bounds__(64 * QPB) hist_kernel(
 }  // namespace
 
 hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, const int32_t* hist_len,
-                       int N, float tau, const double* edges, int B, int32_t* counts, float* mass,
-                       hipStream_t stream) {
+                       int N, float tau, const double* edges, int B, int uniform, int32_t* counts,
+                       float* mass, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
   LaunchScope scope("hist", stream);
   if (B <= 1024) {
     constexpr int qpb = 4;
     const size_t lds = (size_t)qpb * B * 12;
     hipLaunchKernelGGL(hist_kernel<qpb>, dim3((Q + qpb - 1) / qpb), dim3(64 * qpb), lds, stream, ids,
-                       sims, Q, k, hist_len, N, tau, edges, B, counts, mass);
+                       sims, Q, k, hist_len, N, tau, edges, B, uniform, counts, mass);
   } else {
     const size_t lds = (size_t)B * 12;
     hipLaunchKernelGGL(hist_kernel<1>, dim3(Q), dim3(64), lds, stream, ids, sims, Q, k, hist_len,
-                       N, tau, edges, B, counts, mass);
+                       N, tau, edges, B, uniform, counts, mass);
   }
   return hipGetLastError();
 }

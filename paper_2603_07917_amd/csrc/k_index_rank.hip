@@ -34,8 +34,9 @@ __device__ __forceinline__ void load_row(const float* __restrict__ mass, size_t 
 // kAttained also refreshes running requests: with o = bucket *
 // floor(generated / bucket) tokens served, a = o^2 / 2 + I o, the bins with
 // x <= a are ruled out and the rest are shifted down by a, so the result is
-// the index of the remaining cost.
-enum IndexMode { kGivenCost = 0, kFused = 1, kAttained = 2 };
+// the index of the remaining cost. kVariant takes the cost model, the kind
+// of index (Gittins or mean) and a uniform-mixing weight at run time.
+enum IndexMode { kGivenCost = 0, kFused = 1, kAttained = 2, kVariant = 3 };
 // Workgroups per CU the register budget is tuned for (4 waves each).
 template <int C> struct IndexOcc { static constexpr int value = C <= 8 ? 4 : (C == 16 ? 3 : 1); };
 
@@ -46,7 +47,7 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
                                                     const double* __restrict__ repr,
                                                     const int32_t* __restrict__ generated, int bucket,
                                                     int Q, int B, float* __restrict__ index,
-                                                    int32_t* __restrict__ argmin) {
+                                                    int32_t* __restrict__ argmin, IndexVariant var) {
   constexpr bool kFused = kMode != kGivenCost;
   extern __shared__ double repr_s[];               // [B] representatives (fused cost only)
   const int lane = (int)lane_id();
@@ -77,12 +78,30 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     auto support = [&](int j) -> double {
       const int b = b0 + j;
       const bool in = kFull || b < B;
+      if (kMode == kVariant) {
+        const double r = in ? repr_s[b] : 0.0;
+        if (var.cost_model == 1) return r;                       // output length
+        if (var.cost_model == 2) return fma(2.0, r, I);          // input + 2 output
+        return r * fma(0.5, r, I);
+      }
       if (kFused) {
         const double r = in ? repr_s[b] : 0.0;
         return r * fma(0.5, r, I);
       }
       return in ? (double)cost[row + b] : 0.0;
     };
+    if (kMode == kVariant && var.noise > 0.0f) {     // p' = (1 - w) p / sum(p) + w / B
+      double raw = 0.0;
+#pragma unroll
+      for (int j = 0; j < C; ++j) raw += (double)p[j];
+      const double tot = last_lane_f64(wave_incl_scan_dpp_f64(raw));
+      if (tot > 0.0) {
+        const double keep = (1.0 - (double)var.noise) / tot, spread = (double)var.noise / (double)B;
+#pragma unroll
+        for (int j = 0; j < C; ++j)
+          if (kFull || b0 + j < B) p[j] = (float)fma(keep, (double)p[j], spread);
+      }
+    }
     if (kMode == kAttained) {                       // rule out the outcomes already passed
 #pragma unroll
       for (int j = 0; j < C; ++j) p[j] = support(j) > a ? p[j] : 0.0f;
@@ -98,10 +117,16 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     const double f_incl = wave_incl_scan_dpp_f64(lane_f);
     const double f_base = wave_shift_up_dpp_f64(f_incl);
     const double s_base = wave_shift_up_dpp_f64(wave_incl_scan_dpp_f64(lane_s));
-    const double f_total = __longlong_as_double(
-        ((long long)__builtin_amdgcn_readlane((int)((uint64_t)__double_as_longlong(f_incl) >> 32), kWave - 1) << 32) |
-        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)__double_as_longlong(f_incl), kWave - 1));
+    const double f_total = last_lane_f64(f_incl);
     const double t_base = f_total - f_incl;
+    if (kMode == kVariant && var.kind == 1) {        // the mean: sum p x / sum p
+      const double s_incl = s_base + lane_s;
+      if (lane == kWave - 1) {
+        index[q] = f_total > 0.0 ? (float)(s_incl / f_total) : __builtin_inff();
+        if (argmin) argmin[q] = -1;
+      }
+      continue;
+    }
 
     // Branch-free running minimum of n / f by cross-multiplication; the
     // start values (n, f) = (1, 0) lose to the first bin with f > 0, and a
@@ -153,28 +178,33 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
 template <int C, bool kFull, int kMode>
 hipError_t launch_index_v(const float* mass, const float* cost, const int32_t* prompt_len,
                           const double* repr, const int32_t* generated, int bucket, int Q, int B,
-                          float* index, int32_t* argmin, hipStream_t stream) {
+                          float* index, int32_t* argmin, hipStream_t stream, IndexVariant var) {
   const int waves_per_block = 4;
   const int rows_per_wave = 4;
   long waves = ((long)Q + rows_per_wave - 1) / rows_per_wave;
   long blocks = (waves + waves_per_block - 1) / waves_per_block;
   if (blocks > 65535) blocks = 65535;
   if (blocks < 1) blocks = 1;
-  const size_t lds = kMode != kGivenCost ? (size_t)B * sizeof(double) : 0;
+  const size_t lds = kMode != kGivenCost ? (size_t)B * sizeof(double) : 0;   // representatives
   hipLaunchKernelGGL((index_kernel<C, kFull, kMode>), dim3((unsigned)blocks), dim3(64 * waves_per_block),
-                     lds, stream, mass, cost, prompt_len, repr, generated, bucket, Q, B, index, argmin);
+                     lds, stream, mass, cost, prompt_len, repr, generated, bucket, Q, B, index, argmin, var);
   return hipGetLastError();
 }
 
 template <int C>
 hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* prompt_len,
                           const double* repr, const int32_t* generated, int bucket, int Q, int B,
-                          float* index, int32_t* argmin, hipStream_t stream) {
+                          float* index, int32_t* argmin, hipStream_t stream, const IndexVariant* variant) {
   const bool full = B == 64 * C;
-  const int mode = generated ? kAttained : (cost ? kGivenCost : kFused);
+  const int mode = variant ? kVariant : (generated ? kAttained : (cost ? kGivenCost : kFused));
+  const IndexVariant var = variant ? *variant : IndexVariant();
 #define SAGE_INDEX_LAUNCH(FULL, MODE)                                                               \
   return launch_index_v<C, FULL, MODE>(mass, cost, prompt_len, repr, generated, bucket, Q, B, index, \
-                                       argmin, stream)
+                                       argmin, stream, var)
+  if (mode == kVariant) {
+    if (full) SAGE_INDEX_LAUNCH(true, kVariant);
+    SAGE_INDEX_LAUNCH(false, kVariant);
+  }
   if (full) {
     if (mode == kAttained) SAGE_INDEX_LAUNCH(true, kAttained);
     if (mode == kFused) SAGE_INDEX_LAUNCH(true, kFused);
@@ -431,12 +461,13 @@ size_t rank_workspace_bytes(int Q) {
 
 hipError_t launch_index(const float* mass, const float* cost, const int32_t* prompt_len,
                         const double* bin_repr, const int32_t* generated, int bucket, int Q, int B,
-                        float* index, int32_t* argmin, hipStream_t stream) {
+                        float* index, int32_t* argmin, hipStream_t stream, const IndexVariant* variant) {
   if (Q == 0) return hipSuccess;
-  LaunchScope scope(generated ? "index_attained" : "index_scan", stream);
+  LaunchScope scope(variant ? "index_variant" : (generated ? "index_attained" : "index_scan"), stream);
   const int per_lane = (B + kWave - 1) / kWave;
 #define SAGE_INDEX_C(CC) \
-  return launch_index_c<CC>(mass, cost, prompt_len, bin_repr, generated, bucket, Q, B, index, argmin, stream)
+  return launch_index_c<CC>(mass, cost, prompt_len, bin_repr, generated, bucket, Q, B, index, argmin, stream, \
+                            variant)
   if (per_lane <= 1) SAGE_INDEX_C(1);
   if (per_lane <= 2) SAGE_INDEX_C(2);
   if (per_lane <= 4) SAGE_INDEX_C(4);

@@ -257,13 +257,15 @@ SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_e
   hipError_t e = sage::launch_neighbours(queries, Q, hist_emb, N, d, k, plan, workspace, nbr_ids,
                                          nbr_sims, s);
   if (e != hipSuccess) return hip_status(e, "neighbour search launch");
-  e = sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, counts, mass, s);
+  e = sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, 0, counts, mass, s);
   return hip_status(e, "hist launch");
 }
 
-SAGE_API int sage_histogram(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
-                            const int32_t* hist_len, int N, float tau, const double* bin_edges, int B,
-                            int32_t* counts, float* mass, sage_stream_t stream) {
+static int histogram_impl(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
+                          const int32_t* hist_len, int N, float tau, const double* bin_edges, int B,
+                          int weighting, int32_t* counts, float* mass, sage_stream_t stream) {
+  if (weighting != SAGE_WEIGHT_SIMILARITY && weighting != SAGE_WEIGHT_UNIFORM)
+    return fail(SAGE_EINVAL, "weighting=%d is not a SAGE_WEIGHT_* value", weighting);
   if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
   if (k < 1 || k > SAGE_MAX_K) return fail(SAGE_EINVAL, "k=%d outside [1, %d]", k, SAGE_MAX_K);
   if (N < 1) return fail(SAGE_EINVAL, "N=%d must be >= 1", N);
@@ -278,9 +280,24 @@ SAGE_API int sage_histogram(const int32_t* nbr_ids, const float* nbr_sims, int Q
     if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_histogram: misaligned pointer");
   }
   if ((st = check_device()) != SAGE_OK) return st;
-  return hip_status(sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, counts,
-                                      mass, (hipStream_t)stream),
+  return hip_status(sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, weighting,
+                                      counts, mass, (hipStream_t)stream),
                     "hist launch");
+}
+
+SAGE_API int sage_histogram(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
+                            const int32_t* hist_len, int N, float tau, const double* bin_edges, int B,
+                            int32_t* counts, float* mass, sage_stream_t stream) {
+  return histogram_impl(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, SAGE_WEIGHT_SIMILARITY,
+                        counts, mass, stream);
+}
+
+SAGE_API int sage_histogram_variant(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
+                                    const int32_t* hist_len, int N, float tau, const double* bin_edges,
+                                    int B, int weighting, int32_t* counts, float* mass,
+                                    sage_stream_t stream) {
+  return histogram_impl(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, weighting, counts, mass,
+                        stream);
 }
 
 // --------------------------------------------------------- cost / index
@@ -313,6 +330,34 @@ SAGE_API int sage_index(const float* mass, const float* cost, const int32_t* pro
   if (st != SAGE_OK) return st;
   return hip_status(sage::launch_index(mass, cost, prompt_len, bin_repr, nullptr, 1, Q, B, index, argmin_bin,
                                        (hipStream_t)stream),
+                    "index launch");
+}
+
+SAGE_API int sage_index_variant(const float* mass, const int32_t* prompt_len, const double* bin_repr, int Q,
+                                int B, int cost_model, int index_kind, float noise_weight, float* index,
+                                int32_t* argmin_bin, sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (cost_model < SAGE_COST_RESOURCE || cost_model > SAGE_COST_OVERALL)
+    return fail(SAGE_EINVAL, "cost_model=%d is not a SAGE_COST_* value", cost_model);
+  if (index_kind != SAGE_INDEX_GITTINS && index_kind != SAGE_INDEX_MEAN)
+    return fail(SAGE_EINVAL, "index_kind=%d is not a SAGE_INDEX_* value", index_kind);
+  if (!(noise_weight >= 0.0f && noise_weight < 1.0f))
+    return fail(SAGE_EINVAL, "noise_weight=%g outside [0, 1)", (double)noise_weight);
+  if (Q == 0) return ok();
+  if (!mass || !prompt_len || !bin_repr || !index)
+    return fail(SAGE_EINVAL, "sage_index_variant: NULL required pointer");
+  const void* ptrs[] = {mass, prompt_len, bin_repr, index, argmin_bin};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(SAGE_EINVAL, "sage_index_variant: misaligned pointer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  sage::IndexVariant v;
+  v.cost_model = cost_model;
+  v.kind = index_kind;
+  v.noise = noise_weight;
+  return hip_status(sage::launch_index(mass, nullptr, prompt_len, bin_repr, nullptr, 1, Q, B, index,
+                                       argmin_bin, (hipStream_t)stream, &v),
                     "index launch");
 }
 

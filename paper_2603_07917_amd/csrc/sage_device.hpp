@@ -145,6 +145,13 @@ __device__ __forceinline__ double wave_incl_scan_dpp_f64(double x) {
   x += dpp_f64<kDppRowBcast31, 0xc>(0.0, x);
   return x;
 }
+// Lane 63's value, in every lane.
+__device__ __forceinline__ double last_lane_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, kWave - 1);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), kWave - 1);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
 // The inclusive value of the lane below (0 for lane 0): an exclusive prefix.
 __device__ __forceinline__ double wave_shift_up_dpp_f64(double x) { return dpp_f64<kDppWaveShr1>(0.0, x); }
 

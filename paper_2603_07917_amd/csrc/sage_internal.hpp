@@ -47,9 +47,17 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
 hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream);
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
                        float* cost, hipStream_t stream);
+// Index variants: cost model (0 resource, 1 output length, 2 input + 2 output),
+// kind (0 Gittins, 1 mean) and a uniform mixing weight in [0, 1).
+struct IndexVariant {
+  int cost_model = 0;
+  int kind = 0;
+  float noise = 0.0f;
+};
 hipError_t launch_index(const float* mass, const float* cost, const int32_t* prompt_len,
                         const double* bin_repr, const int32_t* generated, int bucket, int Q, int B,
-                        float* index, int32_t* argmin, hipStream_t stream);
+                        float* index, int32_t* argmin, hipStream_t stream,
+                        const IndexVariant* variant = nullptr);
 size_t rank_workspace_bytes(int Q);
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream);
 // Neighbours of every query: ids [Q, k] and sims [Q, k] (sorted, padded).
@@ -63,7 +71,7 @@ hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int li
                              const int* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
                              hipStream_t stream);
 hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, const int32_t* hist_len,
-                       int N, float tau, const double* edges, int B, int32_t* counts, float* mass,
-                       hipStream_t stream);
+                       int N, float tau, const double* edges, int B, int uniform, int32_t* counts,
+                       float* mass, hipStream_t stream);
 
 }  // namespace sage

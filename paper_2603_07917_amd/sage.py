@@ -42,6 +42,8 @@ def load_library():
         "sage_cost": (I, [P, I, P, I, P, S]),
         "sage_index": (I, [P, P, P, P, I, I, P, P, S]),
         "sage_index_attained": (I, [P, P, P, P, I, I, I, P, P, S]),
+        "sage_index_variant": (I, [P, P, P, I, I, I, I, F, P, P, S]),
+        "sage_histogram_variant": (I, [P, P, I, I, P, I, F, P, I, I, P, P, S]),
         "sage_rank_workspace_bytes": (Z, [I]),
         "sage_rank": (I, [P, I, P, P, Z, S]),
         "sage_status_string": (ctypes.c_char_p, [I]),
@@ -195,6 +197,51 @@ def index_attained(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch
                                               _ptr(generated), int(bucket), Q, B, _ptr(g), _ptr(arg),
                                               _stream()))
     return (g, arg) if with_argmin else g
+
+
+COST_MODELS = {"resource": 0, "output": 1, "overall": 2}
+INDEX_KINDS = {"gittins": 0, "mean": 1}
+WEIGHTINGS = {"similarity": 0, "uniform": 1}
+
+
+def index_variant(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor,
+                  cost_model: str = "resource", kind: str = "gittins", noise: float = 0.0,
+                  with_argmin: bool = False, out: Optional[torch.Tensor] = None):
+    """The index under the paper's ablation choices (cost model, Gittins or mean, uniform noise)."""
+    _dev(mass, torch.float32, "mass", 2)
+    _dev(prompt_len, torch.int32, "prompt_len", 1)
+    _dev(bin_repr, torch.float64, "bin_repr", 1)
+    Q, B = mass.shape
+    if prompt_len.shape[0] != Q or bin_repr.shape[0] != B:
+        raise SageError("prompt_len / bin_repr do not match mass")
+    if cost_model not in COST_MODELS or kind not in INDEX_KINDS:
+        raise SageError(f"unknown cost model {cost_model!r} or index kind {kind!r}")
+    g = out if out is not None else torch.empty(Q, dtype=torch.float32, device=mass.device)
+    arg = torch.empty(Q, dtype=torch.int32, device=mass.device) if with_argmin else None
+    _check(load_library().sage_index_variant(_ptr(mass), _ptr(prompt_len), _ptr(bin_repr), Q, B,
+                                             COST_MODELS[cost_model], INDEX_KINDS[kind], float(noise),
+                                             _ptr(g), _ptr(arg), _stream()))
+    return (g, arg) if with_argmin else g
+
+
+def histogram_variant(nbr_ids: torch.Tensor, nbr_sims: torch.Tensor, hist_len: torch.Tensor, tau: float,
+                      bin_edges: torch.Tensor, weighting: str = "uniform"):
+    """sage_histogram with a choice of neighbour weight ("similarity" or "uniform")."""
+    _dev(nbr_ids, torch.int32, "nbr_ids", 2)
+    _dev(nbr_sims, torch.float32, "nbr_sims", 2)
+    _dev(hist_len, torch.int32, "hist_len", 1)
+    _dev(bin_edges, torch.float64, "bin_edges", 1)
+    if weighting not in WEIGHTINGS:
+        raise SageError(f"unknown weighting {weighting!r}")
+    Q, k = nbr_ids.shape
+    B = bin_edges.shape[0] - 1
+    counts = torch.empty((Q, B), dtype=torch.int32, device=nbr_ids.device)
+    mass = torch.empty((Q, B), dtype=torch.float32, device=nbr_ids.device)
+    _check(load_library().sage_histogram_variant(_ptr(nbr_ids), _ptr(nbr_sims), Q, k, _ptr(hist_len),
+                                                 hist_len.shape[0], float(tau), _ptr(bin_edges), B,
+                                                 WEIGHTINGS[weighting], _ptr(counts), _ptr(mass),
+                                                 _stream()))
+    return counts, mass
 
 
 def rank_workspace_bytes(Q: int) -> int:

@@ -34,6 +34,8 @@ def lib():
     lib.sage_rank_workspace_bytes.restype = Z
     lib.sage_index.argtypes = [P, P, P, P, I, I, P, P, P]
     lib.sage_index_attained.argtypes = [P, P, P, P, I, I, I, P, P, P]
+    lib.sage_index_variant.argtypes = [P, P, P, I, I, I, I, F, P, P, P]
+    lib.sage_histogram_variant.argtypes = [P, P, I, I, P, I, F, P, I, I, P, P, P]
     lib.sage_rank.argtypes = [P, I, P, P, Z, P]
     lib.sage_cost.argtypes = [P, I, P, I, P, P]
     lib.sage_histogram.argtypes = [P, P, I, I, P, I, F, P, I, P, P, P]
@@ -123,6 +125,15 @@ def test_index_rank_cost_hist_validation(lib):
     assert lib.sage_index_attained(A, A, A, A + 4, 200, 4, 16, A, None, None) == SAGE_EINVAL
     assert lib.sage_index_attained(A, A, A, A, 200, 4, 5000, A, None, None) == SAGE_EINVAL
     assert lib.sage_index_attained(None, None, None, None, 200, 0, 16, None, None, None) == SAGE_OK
+    # sage_index_variant(mass, prompt_len, bin_repr, Q, B, cost_model, kind, noise, index, argmin, stream)
+    assert lib.sage_index_variant(A, A, A, 4, 16, 3, 0, 0.0, A, None, None) == SAGE_EINVAL    # cost model
+    assert lib.sage_index_variant(A, A, A, 4, 16, 0, 2, 0.0, A, None, None) == SAGE_EINVAL    # kind
+    assert lib.sage_index_variant(A, A, A, 4, 16, 0, 0, 1.0, A, None, None) == SAGE_EINVAL    # noise
+    assert lib.sage_index_variant(A, A, A, 4, 16, 0, 0, -0.1, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index_variant(A, None, A, 4, 16, 0, 0, 0.2, A, None, None) == SAGE_EINVAL
+    assert lib.sage_index_variant(None, None, None, 0, 16, 1, 1, 0.2, None, None, None) == SAGE_OK
+    # sage_histogram_variant(..., weighting, ...)
+    assert lib.sage_histogram_variant(A, A, 4, 8, A, 100, 0.8, A, 16, 2, A, A, None) == SAGE_EINVAL
     assert lib.sage_rank(A, 10, A, A, 0, None) == SAGE_EWORKSPACE
     assert lib.sage_rank(None, 10, A, A, 1 << 20, None) == SAGE_EINVAL
     assert lib.sage_rank(A, -1, A, A, 1 << 20, None) == SAGE_EINVAL

@@ -179,3 +179,51 @@ def test_index_attained_zero_is_the_index_and_argmin(B):
         ok = ~inf
         rows = np.nonzero(ok)[0]
         assert np.all(x[rows, arg[rows]] > a[rows])
+
+
+# --------------------------------------------------------- the paper's ablation variants
+@pytest.mark.parametrize("B", [7, 256, 1024])
+@pytest.mark.parametrize("model", ["resource", "output", "overall"])
+def test_index_variants_vs_oracle(B, model):
+    rng = np.random.default_rng(B + len(model))
+    Q = 400
+    mass = rng.dirichlet(np.full(B, 0.2), size=Q).astype(np.float32)
+    mass[:3] = 0.0                                                 # empty rows
+    plen = rng.integers(8, 8000, size=Q).astype(np.int32)
+    _, r = workloads.log_bins(32768, B)
+    x = oracle.cost_variant(plen, r, model)
+    for noise in (0.0, 0.2):
+        p = oracle.mix_uniform(mass.astype(np.float64), noise) if noise > 0 else mass.astype(np.float64)
+        g = host(sage.index_variant(dev(mass), dev(plen), dev(r), model, "gittins", noise))
+        parity.check_index(g, p, x)
+        m = host(sage.index_variant(dev(mass), dev(plen), dev(r), model, "mean", noise))
+        want = oracle.mean_index(p, x)
+        inf = np.isinf(want)
+        assert np.array_equal(np.isinf(m), inf)
+        rel = np.abs(m[~inf].astype(np.float64) - want[~inf]) / want[~inf]
+        assert rel.max() <= parity.INDEX_RTOL
+    if model == "resource":                                        # the adopted choice is sage_index
+        g0 = host(sage.index(dev(mass), dev(plen), dev(r)))
+        g1 = host(sage.index_variant(dev(mass), dev(plen), dev(r)))
+        assert np.array_equal(g0.view(np.uint32), g1.view(np.uint32))
+
+
+@pytest.mark.parametrize("k,B,tau", [(32, 128, 0.8), (64, 256, 0.5), (100, 37, 0.8)])
+def test_histogram_unweighted_vs_oracle(k, B, tau):
+    rng = np.random.default_rng(k + B)
+    N, Q = 5000, 300
+    edges, _ = workloads.log_bins(8192, B)
+    hist_len = rng.integers(1, 8193, size=N).astype(np.int32)
+    ids = np.stack([rng.choice(N, size=k, replace=False) for _ in range(Q)]).astype(np.int32)
+    ids[:5, k // 2:] = -1
+    sims = np.sort(rng.uniform(0.3, 1.0, size=(Q, k)).astype(np.float32), axis=1)[:, ::-1].copy()
+    sims[5:10] = 0.2                                               # nobody above tau
+    counts, mass = sage.histogram_variant(dev(ids), dev(sims), dev(hist_len), tau, dev(edges), "uniform")
+    counts, mass = host(counts), host(mass)
+    c, m = oracle.histogram(ids, sims, hist_len, edges, tau, weighting="uniform")
+    assert np.array_equal(counts, c)
+    assert np.abs(mass.astype(np.float64) - m).max() <= parity.MASS_TOL
+    # the similarity weighting through the variant entry point is sage_histogram
+    c1, m1 = sage.histogram_variant(dev(ids), dev(sims), dev(hist_len), tau, dev(edges), "similarity")
+    c2, m2 = sage.histogram(dev(ids), dev(sims), dev(hist_len), tau, dev(edges))
+    assert np.array_equal(host(c1), host(c2)) and np.array_equal(host(m1), host(m2))
