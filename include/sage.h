@@ -56,6 +56,25 @@ enum sage_status {
 int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_stream_t stream);
 
 /*
+ * sage_store_insert - FIFO maintenance of the history store (Sec. 3.1: the
+ * records of recently served requests, prompt embedding and output length,
+ * kept in a window updated first-in first-out). The store is a ring of
+ * `capacity` rows: record t (counting every record ever inserted from 0)
+ * lives in row t mod capacity, so the newest record overwrites the oldest,
+ * and the rows in use are [0, min(total, capacity)), contiguous: pass that
+ * many rows to sage_predict.
+ *   emb [n, d] f32 (rounded to bf16, RNE), out_len [n] int32: the batch
+ *   total: records inserted before this batch (kept by the caller; it becomes
+ *          total + n); of a batch larger than the ring, only its last
+ *          `capacity` records are written
+ *   ring_emb [capacity, d] bf16 bits, ring_len [capacity] int32: updated
+ * SAGE_EINVAL: n < 0, d not a positive multiple of 32, capacity < 1,
+ * total < 0, NULL or misaligned pointer.
+ */
+int sage_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
+                      int capacity, uint16_t* ring_emb, int32_t* ring_len, sage_stream_t stream);
+
+/*
  * sage_predict_workspace_bytes - bytes of device workspace sage_predict needs
  * for these sizes (holds the per-stream partial neighbour lists). Returns 0
  * for invalid sizes.

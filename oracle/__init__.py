@@ -5,4 +5,5 @@ the HIP path never imports it and it imports nothing from the product package.
 """
 from .sage_oracle import (attained_service, bf16_to_f64, bin_of, cost, cost_variant,  # noqa: F401
                           gittins, gittins_attained, histogram, mean_index, mix_uniform, predict,
-                          rank, round_to_bf16, schedule, search, similarity, topk, topk_row)
+                          rank, round_to_bf16, schedule, search, similarity, store_insert, topk,
+                          topk_row)

@@ -61,6 +61,21 @@ def bf16_to_f64(bits) -> np.ndarray:
 
 
 # ------------------------------------------------------------- similarity
+def store_insert(ring_bits, ring_len, total: int, emb_f32, out_len, capacity: int):
+    """FIFO history window (Sec. 3.1): record t of all records ever inserted
+    (counting from 0) is kept in row t mod capacity, so each new record
+    replaces the oldest once the window is full. Inserts a batch in order and
+    returns the updated (ring_bits, ring_len, total)."""
+    bits = np.array(ring_bits, dtype=np.uint16, copy=True)
+    lens = np.array(ring_len, dtype=np.int32, copy=True)
+    new_bits = round_to_bf16(np.asarray(emb_f32, dtype=np.float32))
+    for i in range(new_bits.shape[0]):
+        slot = (int(total) + i) % capacity
+        bits[slot] = new_bits[i]
+        lens[slot] = int(out_len[i])
+    return bits, lens, int(total) + new_bits.shape[0]
+
+
 def similarity(q_bits, h_bits) -> np.ndarray:
     """s[q, n] = sum_t Q[q, t] * H[n, t] over the stored bf16 values, in fp64.
 

@@ -28,6 +28,30 @@ __global__ void __launch_bounds__(256) ingest_bf16_kernel(const float* __restric
     dst[i] = bf16_rne(src[i]);
 }
 
+// FIFO insert into the history ring: record i of the batch (only the last
+// `cap` of the batch survive) goes to slot (total + i) mod cap, embedding
+// rounded to bf16 (RNE), length copied. One thread per 8 embedding values.
+__global__ void __launch_bounds__(256) store_insert_kernel(const float* __restrict__ emb,
+                                                           const int32_t* __restrict__ out_len, int n, int d,
+                                                           int first, long long total, int cap,
+                                                           uint16_t* __restrict__ ring_emb,
+                                                           int32_t* __restrict__ ring_len) {
+  const int per_row = d / 8;
+  const size_t work = (size_t)(n - first) * per_row;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t w = (size_t)blockIdx.x * blockDim.x + threadIdx.x; w < work; w += stride) {
+    const int i = first + (int)(w / per_row);
+    const int c = (int)(w % per_row) * 8;
+    const size_t slot = (size_t)((total + i) % cap);
+    const float4 a = *reinterpret_cast<const float4*>(emb + (size_t)i * d + c);
+    const float4 b = *reinterpret_cast<const float4*>(emb + (size_t)i * d + c + 4);
+    ushort4* dst = reinterpret_cast<ushort4*>(ring_emb + slot * d + c);
+    dst[0] = make_ushort4(bf16_rne(a.x), bf16_rne(a.y), bf16_rne(a.z), bf16_rne(a.w));
+    dst[1] = make_ushort4(bf16_rne(b.x), bf16_rne(b.y), bf16_rne(b.z), bf16_rne(b.w));
+    if (c == 0) ring_len[slot] = out_len[i];
+  }
+}
+
 // x[q, b] = r_b^2 / 2 + I_q * r_b in fp64, rounded once to fp32.
 __global__ void __launch_bounds__(256) cost_kernel(const int32_t* __restrict__ prompt_len, int Q,
                                                    const double* __restrict__ repr, int B,
@@ -56,6 +80,17 @@ hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStre
   LaunchScope scope("ingest_bf16", stream);
   hipLaunchKernelGGL(ingest_bf16_kernel, dim3(grid_for(n / 4 + 1, 256, 8192)), dim3(256), 0, stream,
                      src, n, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
+                               int cap, uint16_t* ring_emb, int32_t* ring_len, hipStream_t stream) {
+  const int first = n > cap ? n - cap : 0;     // earlier records of the batch would be evicted at once
+  const size_t work = (size_t)(n - first) * (d / 8);
+  if (work == 0) return hipSuccess;
+  LaunchScope scope("store_insert", stream);
+  hipLaunchKernelGGL(store_insert_kernel, dim3(grid_for(work, 256, 8192)), dim3(256), 0, stream, emb, out_len,
+                     n, d, first, total, cap, ring_emb, ring_len);
   return hipGetLastError();
 }
 

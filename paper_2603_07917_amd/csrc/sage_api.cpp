@@ -211,6 +211,25 @@ SAGE_API int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_st
   return hip_status(sage::launch_ingest_bf16(src, n, dst, (hipStream_t)stream), "ingest_bf16 launch");
 }
 
+SAGE_API int sage_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
+                               int capacity, uint16_t* ring_emb, int32_t* ring_len, sage_stream_t stream) {
+  if (n < 0) return fail(SAGE_EINVAL, "n=%d is negative", n);
+  if (d < 32 || d % 32 != 0) return fail(SAGE_EINVAL, "d=%d must be a positive multiple of 32", d);
+  if (capacity < 1) return fail(SAGE_EINVAL, "capacity=%d must be >= 1", capacity);
+  if (total < 0) return fail(SAGE_EINVAL, "total=%lld is negative", total);
+  if (n == 0) return ok();
+  const void* ptrs[] = {emb, out_len, ring_emb, ring_len};
+  for (const void* p : ptrs) {
+    if (!p) return fail(SAGE_EINVAL, "sage_store_insert: NULL pointer");
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_store_insert: misaligned pointer");
+  }
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_store_insert(emb, out_len, n, d, total, capacity, ring_emb, ring_len,
+                                              (hipStream_t)stream),
+                    "store_insert launch");
+}
+
 // ------------------------------------------------------------- predict
 namespace {
 int check_predict_sizes(int Q, int N, int d, int k, int B) {

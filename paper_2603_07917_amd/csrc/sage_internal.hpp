@@ -45,6 +45,8 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
 // Launchers: each enqueues kernels on `stream` and returns the HIP status of
 // the launch (hipSuccess or the first error).
 hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream);
+hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
+                               int cap, uint16_t* ring_emb, int32_t* ring_len, hipStream_t stream);
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
                        float* cost, hipStream_t stream);
 // Index variants: cost model (0 resource, 1 output length, 2 input + 2 output),

@@ -44,6 +44,7 @@ def load_library():
         "sage_index_attained": (I, [P, P, P, P, I, I, I, P, P, S]),
         "sage_index_variant": (I, [P, P, P, I, I, I, I, F, P, P, S]),
         "sage_histogram_variant": (I, [P, P, I, I, P, I, F, P, I, I, P, P, S]),
+        "sage_store_insert": (I, [P, P, I, I, ctypes.c_longlong, I, P, P, S]),
         "sage_rank_workspace_bytes": (Z, [I]),
         "sage_rank": (I, [P, I, P, P, Z, S]),
         "sage_status_string": (ctypes.c_char_p, [I]),
@@ -312,6 +313,50 @@ class Store:
             self._rank_ws = torch.empty(need, dtype=torch.uint8, device=g.device)
         order = rank(g, workspace=self._rank_ws, out=None if out is None else out[5])
         return ids, sims, counts, mass, g, order
+
+
+def store_insert(emb: torch.Tensor, out_len: torch.Tensor, total: int, ring_emb: torch.Tensor,
+                 ring_len: torch.Tensor) -> int:
+    """FIFO insert of a batch of served records into a history ring; returns the new total."""
+    _dev(emb, torch.float32, "emb", 2)
+    _dev(out_len, torch.int32, "out_len", 1)
+    _dev(ring_emb, torch.bfloat16, "ring_emb", 2)
+    _dev(ring_len, torch.int32, "ring_len", 1)
+    n, d = emb.shape
+    cap = ring_emb.shape[0]
+    if out_len.shape[0] != n or ring_emb.shape[1] != d or ring_len.shape[0] != cap:
+        raise SageError("emb / out_len / ring shapes do not match")
+    _check(load_library().sage_store_insert(_ptr(emb), _ptr(out_len), n, d, int(total), cap,
+                                            _ptr(ring_emb), _ptr(ring_len), _stream()))
+    return int(total) + n
+
+
+class RingStore(Store):
+    """A history store kept as a FIFO window of `capacity` records: served
+    requests are inserted with `insert`, the oldest is overwritten once the
+    window is full, and predictions search the rows in use."""
+
+    def __init__(self, capacity: int, d: int, bin_edges: torch.Tensor, bin_repr: torch.Tensor, k: int,
+                 tau: float = 0.8):
+        dev = bin_edges.device
+        self.ring_emb = torch.zeros((capacity, d), dtype=torch.bfloat16, device=dev)
+        self.ring_len = torch.zeros(capacity, dtype=torch.int32, device=dev)
+        self.total = 0
+        super().__init__(self.ring_emb[:1], self.ring_len[:1], bin_edges, bin_repr, k, tau)
+
+    @property
+    def rows(self) -> int:
+        return min(self.total, self.ring_emb.shape[0])
+
+    def insert(self, emb: torch.Tensor, out_len: torch.Tensor):
+        self.total = store_insert(emb.contiguous(), out_len, self.total, self.ring_emb, self.ring_len)
+        self.hist_emb = self.ring_emb[:self.rows]
+        self.hist_len = self.ring_len[:self.rows]
+
+    def predict(self, queries: torch.Tensor, out=None):
+        if self.total == 0:
+            raise SageError("the history window is empty")
+        return super().predict(queries, out=out)
 
 
 class Queue:

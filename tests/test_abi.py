@@ -36,6 +36,7 @@ def lib():
     lib.sage_index_attained.argtypes = [P, P, P, P, I, I, I, P, P, P]
     lib.sage_index_variant.argtypes = [P, P, P, I, I, I, I, F, P, P, P]
     lib.sage_histogram_variant.argtypes = [P, P, I, I, P, I, F, P, I, I, P, P, P]
+    lib.sage_store_insert.argtypes = [P, P, I, I, ctypes.c_longlong, I, P, P, P]
     lib.sage_rank.argtypes = [P, I, P, P, Z, P]
     lib.sage_cost.argtypes = [P, I, P, I, P, P]
     lib.sage_histogram.argtypes = [P, P, I, I, P, I, F, P, I, P, P, P]
@@ -134,6 +135,12 @@ def test_index_rank_cost_hist_validation(lib):
     assert lib.sage_index_variant(None, None, None, 0, 16, 1, 1, 0.2, None, None, None) == SAGE_OK
     # sage_histogram_variant(..., weighting, ...)
     assert lib.sage_histogram_variant(A, A, 4, 8, A, 100, 0.8, A, 16, 2, A, A, None) == SAGE_EINVAL
+    # sage_store_insert(emb, out_len, n, d, total, capacity, ring_emb, ring_len, stream)
+    assert lib.sage_store_insert(A, A, 4, 48, 0, 10, A, A, None) == SAGE_EINVAL       # d % 32
+    assert lib.sage_store_insert(A, A, 4, 64, 0, 0, A, A, None) == SAGE_EINVAL        # capacity
+    assert lib.sage_store_insert(A, A, 4, 64, -1, 10, A, A, None) == SAGE_EINVAL      # total
+    assert lib.sage_store_insert(A, None, 4, 64, 0, 10, A, A, None) == SAGE_EINVAL
+    assert lib.sage_store_insert(None, None, 0, 64, 0, 10, None, None, None) == SAGE_OK
     assert lib.sage_rank(A, 10, A, A, 0, None) == SAGE_EWORKSPACE
     assert lib.sage_rank(None, 10, A, A, 1 << 20, None) == SAGE_EINVAL
     assert lib.sage_rank(A, -1, A, A, 1 << 20, None) == SAGE_EINVAL

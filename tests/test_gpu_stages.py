@@ -227,3 +227,33 @@ def test_histogram_unweighted_vs_oracle(k, B, tau):
     c1, m1 = sage.histogram_variant(dev(ids), dev(sims), dev(hist_len), tau, dev(edges), "similarity")
     c2, m2 = sage.histogram(dev(ids), dev(sims), dev(hist_len), tau, dev(edges))
     assert np.array_equal(host(c1), host(c2)) and np.array_equal(host(m1), host(m2))
+
+
+# ---------------------------------------------------------- history window (FIFO store)
+def test_store_insert_fifo_bit_exact_and_predict():
+    rng = np.random.default_rng(17)
+    cap, d = 1000, 64
+    edges, r = workloads.log_bins(4096, 32)
+    ring = sage.RingStore(cap, d, dev(edges), dev(r), k=16, tau=0.8)
+    bits = np.zeros((cap, d), np.uint16)
+    lens = np.zeros(cap, np.int32)
+    total = 0
+    w = workloads.small_predict(Q=20, N=4000, d=d, k=16, B=32, seed=3, clusters=5)
+    for n in [1, 299, 0, 700, 1, 1500, 333]:
+        a = rng.integers(0, 4000 - n) if n < 4000 else 0
+        emb, out = w.hist_emb[a:a + n], w.hist_len[a:a + n]
+        ring.insert(dev(emb.reshape(n, d)), dev(out))
+        bits, lens, total = oracle.store_insert(bits, lens, total, emb.reshape(n, d), out, cap)
+        assert ring.total == total and ring.rows == min(total, cap)
+        assert np.array_equal(host(ring.ring_emb.view(torch.int16)).view(np.uint16)[:ring.rows], bits[:ring.rows])
+        assert np.array_equal(host(ring.ring_len)[:ring.rows], lens[:ring.rows])
+    # predictions over the window equal those over the same rows given directly
+    q = dev(w.queries)
+    a_out = [host(t) for t in ring.predict(q)]
+    direct = sage.Store(ring.ring_emb[:ring.rows].clone(), ring.ring_len[:ring.rows].clone(),
+                        dev(edges), dev(r), 16, 0.8)
+    b_out = [host(t) for t in direct.predict(q)]
+    for x, y in zip(a_out, b_out):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+    S = oracle.similarity(oracle.round_to_bf16(w.queries), bits)
+    parity.check_topk(a_out[0], a_out[1], S, 16)
