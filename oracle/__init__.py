@@ -7,3 +7,5 @@ from .sage_oracle import (attained_service, bf16_to_f64, bin_of, cost, cost_vari
                           gittins, gittins_attained, histogram, mean_index, mix_uniform, predict,
                           rank, round_to_bf16, schedule, search, similarity, store_insert, topk,
                           topk_row)
+from .sage_sim import (POLICIES, policy_order, refresh_levels, service_cost, simulate,  # noqa: F401
+                       simulate_policy)

@@ -37,7 +37,7 @@ import numpy as np
 SEED_BASE = 260307917
 # Order in which child streams are spawned; never reorder (changes every input).
 STREAMS = ("centres", "cluster_params", "assignment", "noise", "lengths",
-           "queries", "prompt_lengths", "masses", "standing", "attained")
+           "queries", "prompt_lengths", "masses", "standing", "attained", "trace")
 
 
 def streams(config_id: int, seed_base: int = SEED_BASE) -> dict:
@@ -273,6 +273,44 @@ def generated_tokens(config_id: int, Q: int, L_max: int, running: float = 0.5,
     run = r.random(Q) < running
     u = r.random(Q)
     return np.where(run, np.floor(L_max * u * u / 4.0), 0).astype(np.int32)
+
+
+@dataclass
+class TraceInputs:
+    """A stream of requests for the queueing simulation."""
+    arrival: np.ndarray       # [R] float64 seconds, non-decreasing (Poisson process)
+    queries: np.ndarray       # [R, d] float32 prompt embeddings
+    cluster: np.ndarray       # [R] int32 (-1 for noise requests)
+    prompt_len: np.ndarray    # [R] int32 input lengths I
+    output_len: np.ndarray    # [R] int32 true output lengths O (unknown to the scheduler)
+    rps: float
+
+
+def make_trace(spec: PredictSpec, config_id: int, R: int, rps: float,
+               seed_base: int = SEED_BASE) -> TraceInputs:
+    """R requests of the mixture behind a history store, arriving as a Poisson
+    process of rate ``rps`` (Sec. 4.1 draws submission intervals from a
+    Poisson process). Each request belongs to a cluster drawn like the store's
+    rows; its true output length follows that cluster's lognormal law, so the
+    store's neighbours of its prompt carry its length distribution. Drawn
+    from the "trace" stream; the cluster centres and laws are the store's."""
+    r = streams(config_id, seed_base)
+    centres = _unit_rows(r["centres"].standard_normal((spec.clusters, spec.d)))
+    cp = r["cluster_params"]
+    mus = cp.uniform(*spec.mu_range, size=spec.clusters)
+    ss = cp.uniform(*spec.s_range, size=spec.clusters)
+    probs = _cluster_probs(spec, cp)
+    rt = r["trace"]
+    arrival = np.cumsum(rt.exponential(1.0 / float(rps), size=R))
+    cluster = rt.choice(spec.clusters, size=R, p=probs).astype(np.int32)
+    noise = rt.random(R) < spec.noise_frac
+    law = np.where(noise, rt.integers(0, spec.clusters, size=R), cluster)
+    cluster = np.where(noise, -1, cluster).astype(np.int32)
+    queries = _points(rt, centres, cluster, spec, noise)
+    prompt_len = _prompt_lengths(rt, spec.prompt, R)
+    z = rt.standard_normal(R)
+    output_len = np.clip(np.rint(np.exp(mus[law] + ss[law] * z)), 1, spec.L_max).astype(np.int32)
+    return TraceInputs(arrival, queries, cluster, prompt_len, output_len, float(rps))
 
 
 def make_config(config_id: int, **overrides):

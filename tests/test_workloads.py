@@ -1,5 +1,6 @@
 """The seeded generators: determinism, shapes and ranges (CPU only)."""
 import numpy as np
+import pytest
 
 from paper_2603_07917_amd import workloads
 
@@ -43,3 +44,19 @@ def test_noise_and_zipf_options():
     assert 0.05 < np.mean(w.hist_cluster == -1) < 0.15
     counts = np.bincount(w.hist_cluster[w.hist_cluster >= 0], minlength=50)
     assert counts.max() > 5 * np.median(counts)  # skewed popularity
+
+
+def test_trace_is_poisson_and_deterministic():
+    from scipy.stats import kstest
+    spec = workloads.PredictSpec(Q=1, N=1, d=32, clusters=16, mu_range=(3.0, 6.0), s_range=(0.5, 1.0),
+                                 L_max=4096, k=1, B=16)
+    t = workloads.make_trace(spec, 77, 20000, 8.0)
+    gaps = np.diff(np.concatenate([[0.0], t.arrival]))
+    assert np.all(gaps >= 0)
+    assert gaps.mean() == pytest.approx(1 / 8.0, rel=0.03)
+    assert kstest(gaps, "expon", args=(0, 1 / 8.0)).pvalue > 1e-3
+    assert t.output_len.min() >= 1 and t.output_len.max() <= 4096
+    assert t.queries.shape == (20000, 32) and t.prompt_len.shape == (20000,)
+    np.testing.assert_allclose(np.linalg.norm(t.queries, axis=1), 1.0, atol=1e-5)
+    t2 = workloads.make_trace(spec, 77, 20000, 8.0)
+    assert np.array_equal(t.arrival, t2.arrival) and np.array_equal(t.output_len, t2.output_len)
