@@ -34,6 +34,18 @@ def oracle_scores(w, rows=None):
     return oracle.similarity(qb, oracle.round_to_bf16(w.hist_emb))
 
 
+def check_decision(w, rows, ids, sims, counts, mass, g, order, k, tau):
+    """Predict, index and rank of the sampled rows against the oracle's own
+    results from the same seeded inputs; returns the number of clean rows."""
+    S = oracle_scores(w, rows)
+    clean, mass_o, delta = parity.check_predict(ids[rows], sims[rows], counts[rows], mass[rows], S,
+                                                w.hist_len, w.bin_edges, tau, k)
+    x = oracle.cost(w.prompt_len[rows], w.bin_repr)
+    parity.check_index_downstream(g[rows], mass_o, x, delta, np.nonzero(clean)[0])
+    parity.check_sorted_stably(order, g)
+    return int(clean.sum())
+
+
 # (Q, N, d, k, B): several query tiles with a ragged tail, history chunks and
 # 256-row steps with ragged ends, d with a half 64-wide slice, every list length.
 CASES = [
@@ -56,8 +68,7 @@ def test_predict_small_vs_oracle(Q, N, d, k, B):
     w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=B, seed=Q + N + d + k, clusters=6)
     ids, sims, counts, mass = run_predict(w, k)
     S = oracle_scores(w)
-    parity.check_topk(ids, sims, S, k)
-    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, 0.8)
+    parity.check_predict(ids, sims, counts, mass, S, w.hist_len, w.bin_edges, 0.8, k)
 
 
 def test_predict_duplicate_rows_lower_id_first():
@@ -87,9 +98,8 @@ def test_predict_candidate_overflow_takes_exact_fallback():
     w.queries[:6] = h[6000]
     ids, sims, counts, mass = run_predict(w, 8)
     S = oracle_scores(w)
-    parity.check_topk(ids, sims, S, 8)
     assert list(ids[0]) == list(range(8))          # all tied: lowest indices first
-    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, 0.8)
+    parity.check_predict(ids, sims, counts, mass, S, w.hist_len, w.bin_edges, 0.8, 8)
 
 
 def test_predict_tau_fallback_and_all_same_length():
@@ -98,7 +108,7 @@ def test_predict_tau_fallback_and_all_same_length():
     ids, sims, counts, mass = run_predict(w, 16, tau=1.0)      # nobody reaches tau = 1
     b = oracle.bin_of([777], w.bin_edges)[0]
     assert np.all(counts[:, b] == 16) and np.all(mass[:, b] == 1.0)
-    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, 1.0)
+    parity.check_predict(ids, sims, counts, mass, oracle_scores(w), w.hist_len, w.bin_edges, 1.0, 16)
 
 
 def test_predict_deterministic():
@@ -112,14 +122,12 @@ def test_predict_deterministic():
 def test_config1_end_to_end():
     w = workloads.make_config(1)
     spec = w.spec
-    ids, sims, counts, mass = run_predict(w, spec.k, spec.tau)
-    S = oracle_scores(w)
-    equal = parity.check_topk(ids, sims, S, spec.k)
-    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
-    g = host(sage.index(dev(mass), dev(w.prompt_len), dev(w.bin_repr)))
-    parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
-    parity.check_rank(host(sage.rank(dev(g))), g)
-    print(f"config 1: {equal}/{spec.Q} queries with the oracle's exact neighbour set", flush=True)
+    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
+                       spec.k, spec.tau)
+    out = store.decide(dev(w.queries), dev(w.prompt_len))
+    ids, sims, counts, mass, g, order = [host(t) for t in out]
+    clean = check_decision(w, np.arange(spec.Q), ids, sims, counts, mass, g, order, spec.k, spec.tau)
+    print(f"config 1: {clean}/{spec.Q} queries compared through the index", flush=True)
 
 
 def test_config2_full_size_sampled():
@@ -133,12 +141,8 @@ def test_config2_full_size_sampled():
     rng = np.random.default_rng(2)
     rows = np.sort(rng.choice(spec.Q, size=48, replace=False))
     rows = np.unique(np.concatenate([rows, [0, spec.Q - 1]]))
-    S = oracle_scores(w, rows)
-    equal = parity.check_topk(ids[rows], sims[rows], S, spec.k)
-    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
-    parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
-    parity.check_rank(order, g)
-    print(f"config 2: {equal}/{len(rows)} sampled queries with the exact neighbour set", flush=True)
+    clean = check_decision(w, rows, ids, sims, counts, mass, g, order, spec.k, spec.tau)
+    print(f"config 2: {clean}/{len(rows)} sampled queries compared through the index", flush=True)
 
 
 def test_config3_full_size_sampled():
@@ -153,9 +157,5 @@ def test_config3_full_size_sampled():
     noise_q = np.nonzero(w.query_cluster < 0)[0]
     rows = np.concatenate([rng.choice(spec.Q, size=20, replace=False), noise_q[:4], [0, spec.Q - 1]])
     rows = np.unique(rows)
-    S = oracle_scores(w, rows)
-    equal = parity.check_topk(ids[rows], sims[rows], S, spec.k)
-    parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
-    parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
-    parity.check_rank(order, g)
-    print(f"config 3: {equal}/{len(rows)} sampled queries with the exact neighbour set", flush=True)
+    clean = check_decision(w, rows, ids, sims, counts, mass, g, order, spec.k, spec.tau)
+    print(f"config 3: {clean}/{len(rows)} sampled queries compared through the index", flush=True)

