@@ -231,6 +231,52 @@ size_t sage_rank_workspace_bytes(int Q);
 int sage_rank(const float* index, int Q, int32_t* order,
               void* workspace, size_t workspace_bytes, sage_stream_t stream);
 
+/*
+ * sage_simulate - replay of a request trace against a queue served in a
+ * given priority order: a discrete-event simulation run on the HOST (all
+ * pointers are host pointers, nothing is enqueued on a stream). It measures
+ * the paper's metric, the time-to-last-token (TTLT = finish - arrival,
+ * Sec. 2), of an ordering.
+ *
+ * Model. Requests arrive at arrival[r] (Sec. 4.1 uses Poisson arrivals).
+ * Request r needs C = O^2/2 + I*O cost units (the unified cost of Sec. 3.2
+ * at its true lengths I = prompt_len[r], O = output_len[r]); after g
+ * generated tokens it has received a(g) = g^2/2 + I*g. `servers` identical
+ * servers each run one request at a time at `rate` cost units per second.
+ * After every event instant (completions, then bucket boundaries, then
+ * arrivals at that instant) the `servers` admitted requests with the
+ * smallest keys run; a running request that drops out is preempted and keeps
+ * its service (preemption is enabled at negligible cost, Sec. 3.3). At most
+ * queue_cap requests wait besides those running (Sec. 4.4 buffers up to
+ * 1,000); later arrivals wait outside in arrival order and are admitted as
+ * requests finish.
+ *
+ * Keys. order[0 .. levels*R) is a permutation of the entries e = k*R + r,
+ * best first (sage_rank's output over an index table with one row per
+ * level); request r's key is the position of entry (k, r), k being the
+ * number of bucket boundaries it has crossed (one every `bucket` generated
+ * tokens, Sec. 3.3 refreshes the index only there). bucket = 0: keys are
+ * never refreshed and levels must be 1 (FCFS, Mean, Gittins at arrival);
+ * bucket > 0: levels >= ceil(max O / bucket). Positions informed .. levels*R
+ * of the order hold entries without information: a refreshed index of +inf
+ * (sage_index_attained's value when no predicted mass lies above the service
+ * received) ranks last; a request reaching such a level keeps its key.
+ * Pass informed = levels * R when every entry is meaningful.
+ *
+ *   arrival [R] f64 seconds, finite and non-decreasing
+ *   prompt_len [R] int32 >= 0, output_len [R] int32 >= 1
+ *   order [levels * R] int32, 0 <= informed <= levels * R
+ *   servers >= 1, rate > 0 finite, queue_cap >= 0
+ *   finish [R] f64 out (completion time), preemptions [R] int32 out or NULL
+ * SAGE_EINVAL for a NULL required pointer, R < 0, levels * R >= 2^31, a
+ * decreasing or non-finite arrival, out-of-range lengths, too few levels, an
+ * order that is not a permutation, or bad servers / rate / queue_cap. R = 0
+ * is a no-op. The caller owns every buffer; nothing is retained.
+ */
+int sage_simulate(const double* arrival, const int32_t* prompt_len, const int32_t* output_len, int R,
+                  const int32_t* order, int levels, int informed, int bucket, int servers, double rate,
+                  int queue_cap, double* finish, int32_t* preemptions);
+
 /* Static, thread-safe name of a status code. Host pointer. */
 const char* sage_status_string(int status);
 

@@ -19,6 +19,13 @@ boundaries (a boundary every ``bucket`` generated tokens, Sec. 3.3: the index
 of a running request is refreshed only there). Without refreshing
 (``bucket = 0``) every request keeps its level-0 entry. The keys are the
 positions of the entries in ``order``, the queue order produced by ranking.
+Entries at positions ``informed`` and beyond carry no information: a
+refreshed index is +inf when the predicted distribution has no mass left
+above the service already received (every predicted length has been
+outlived), and +inf ranks last. Reaching such a level leaves the request's
+key as it was (reading: the refresh has no remaining-cost distribution to
+act on, so the last index stands; ranking such requests last instead starves
+them behind every newcomer).
 
 Readings where the paper is silent (each listed with the simulator's design):
 
@@ -66,7 +73,7 @@ def _served(I: int, g: int) -> float:
 
 
 def simulate(arrival, prompt_len, output_len, order, *, servers: int, rate: float,
-             queue_cap: int, bucket: int = 0, levels: int = 1):
+             queue_cap: int, bucket: int = 0, levels: int = 1, informed: int | None = None):
     """Event-by-event simulation; returns (finish [R] float64, preemptions [R] int32)."""
     arrival = [float(v) for v in np.asarray(arrival, dtype=np.float64)]
     I = [int(v) for v in np.asarray(prompt_len)]
@@ -82,9 +89,12 @@ def simulate(arrival, prompt_len, output_len, order, *, servers: int, rate: floa
     key = [0] * (levels * R)
     for pos, e in enumerate(order.tolist()):
         key[e] = pos
+    if informed is None:
+        informed = levels * R
     C = [O[r] * O[r] / 2.0 + I[r] * O[r] for r in range(R)]
 
     level = [0] * R             # boundaries crossed
+    cur = key[:R]               # current key: the level-0 entry until a refresh replaces it
     attained = [0.0] * R        # service at the last stop (0 before the first start)
     finish = [0.0] * R
     preempt = [0] * R
@@ -94,7 +104,7 @@ def simulate(arrival, prompt_len, output_len, order, *, servers: int, rate: floa
     pool = 0                    # admitted and unfinished
 
     def priority(r):
-        return key[level[r] * R + r]
+        return cur[r]
 
     def start(r, t):
         a0 = attained[r]
@@ -124,6 +134,8 @@ def simulate(arrival, prompt_len, output_len, order, *, servers: int, rate: floa
             if seg[4] == t:
                 level[r] += 1
                 attained[r] = seg[2]
+                if key[level[r] * R + r] < informed:
+                    cur[r] = key[level[r] * R + r]
                 start(r, t)
         while arrived < R and arrival[arrived] == t:     # arrivals
             arrived += 1
@@ -156,7 +168,7 @@ def refresh_levels(output_len, bucket: int) -> int:
 
 
 def policy_order(policy: str, arrival, mass, prompt_len, bin_repr, output_len=None, bucket: int = 0):
-    """Queue order of a policy, as (order, levels).
+    """Queue order of a policy, as (order, levels, informed).
 
     * ``fcfs``: arrival order (vLLM's default, Sec. 2);
     * ``mean``: the mean of the predicted cost distribution (Sec. 4.3);
@@ -164,35 +176,36 @@ def policy_order(policy: str, arrival, mass, prompt_len, bin_repr, output_len=No
       paper's "Gittins-minus" ablation, Sec. 4.3);
     * ``gittins``: the Gittins index of the remaining cost, refreshed at every
       bucket boundary (Sec. 3.3); the table's level k holds the index after
-      k * bucket generated tokens.
+      k * bucket generated tokens, and ``informed`` counts its finite values.
 
     The index values order the queue; the order is taken on their fp32
     values (the precision the scheduling kernels emit), ties to the lower
     entry id.
     """
+    R = len(prompt_len)
     if policy == "fcfs":
-        return rank(np.asarray(arrival, dtype=np.float64)), 1
+        return rank(np.asarray(arrival, dtype=np.float64)), 1, R
     x = cost(prompt_len, bin_repr)
     if policy == "mean":
-        return rank(mean_index(mass, x).astype(np.float32)), 1
+        return rank(mean_index(mass, x).astype(np.float32)), 1, R
     if policy == "gittins-static":
-        return rank(gittins(mass, x)[0].astype(np.float32)), 1
+        return rank(gittins(mass, x)[0].astype(np.float32)), 1, R
     if policy == "gittins":
         L = refresh_levels(output_len, bucket)
-        R = len(prompt_len)
         table = np.empty((L, R), dtype=np.float32)
         for k in range(L):
             a = attained_service(prompt_len, np.full(R, k * bucket), bucket)
             table[k] = gittins_attained(mass, x, a)[0].astype(np.float32)
-        return rank(table.ravel()), L
+        return rank(table.ravel()), L, int(np.isfinite(table).sum())
     raise ValueError(f"policy_order: unknown policy {policy!r}")
 
 
 def simulate_policy(policy: str, arrival, mass, prompt_len, bin_repr, output_len, *, servers: int,
                     rate: float, queue_cap: int, bucket: int = 200):
     """Order the queue by `policy` and simulate; returns (ttlt, preemptions)."""
-    order, levels = policy_order(policy, arrival, mass, prompt_len, bin_repr, output_len, bucket)
+    order, levels, informed = policy_order(policy, arrival, mass, prompt_len, bin_repr, output_len,
+                                           bucket)
     b = bucket if policy == "gittins" else 0
     finish, pre = simulate(arrival, prompt_len, output_len, order, servers=servers, rate=rate,
-                           queue_cap=queue_cap, bucket=b, levels=levels)
+                           queue_cap=queue_cap, bucket=b, levels=levels, informed=informed)
     return finish - np.asarray(arrival, dtype=np.float64), pre

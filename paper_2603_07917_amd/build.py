@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsage.so")
 
-SOURCES = ["sage_api.cpp", "k_elementwise.hip", "k_index_rank.hip", "k_hist.hip",
+SOURCES = ["sage_api.cpp", "sim.cpp", "k_elementwise.hip", "k_index_rank.hip", "k_hist.hip",
            "k_topk_merge.hip", "k_sim_topk.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -416,3 +416,44 @@ SAGE_API int sage_rank(const float* index, int Q, int32_t* order, void* workspac
   if (st != SAGE_OK) return st;
   return hip_status(sage::launch_rank(index, Q, order, workspace, (hipStream_t)stream), "rank launch");
 }
+
+// ------------------------------------------------------------ simulate
+SAGE_API int sage_simulate(const double* arrival, const int32_t* prompt_len, const int32_t* output_len,
+                           int R, const int32_t* order, int levels, int informed, int bucket,
+                           int servers, double rate, int queue_cap, double* finish,
+                           int32_t* preemptions) {
+  if (R < 0) return fail(SAGE_EINVAL, "R=%d is negative", R);
+  if (levels < 1) return fail(SAGE_EINVAL, "levels=%d must be >= 1", levels);
+  if ((long long)levels * R > 0x7fffffffLL)
+    return fail(SAGE_EINVAL, "levels * R = %lld exceeds 2^31 - 1", (long long)levels * R);
+  if (informed < 0 || (long long)informed > (long long)levels * R)
+    return fail(SAGE_EINVAL, "informed=%d outside [0, levels * R]", informed);
+  if (bucket < 0) return fail(SAGE_EINVAL, "bucket=%d is negative", bucket);
+  if (bucket == 0 && levels != 1) return fail(SAGE_EINVAL, "levels=%d without refreshing (bucket 0)", levels);
+  if (servers < 1) return fail(SAGE_EINVAL, "servers=%d must be >= 1", servers);
+  if (!(rate > 0.0) || !std::isfinite(rate)) return fail(SAGE_EINVAL, "rate=%g must be positive and finite", rate);
+  if (queue_cap < 0) return fail(SAGE_EINVAL, "queue_cap=%d is negative", queue_cap);
+  if (R == 0) return ok();
+  if (!arrival || !prompt_len || !output_len || !order || !finish)
+    return fail(SAGE_EINVAL, "sage_simulate: NULL pointer");
+  for (int r = 0; r < R; ++r) {
+    if (!std::isfinite(arrival[r])) return fail(SAGE_EINVAL, "arrival[%d] is not finite", r);
+    if (r > 0 && arrival[r] < arrival[r - 1]) return fail(SAGE_EINVAL, "arrivals decrease at %d", r);
+    if (prompt_len[r] < 0) return fail(SAGE_EINVAL, "prompt_len[%d]=%d is negative", r, prompt_len[r]);
+    if (output_len[r] < 1) return fail(SAGE_EINVAL, "output_len[%d]=%d must be >= 1", r, output_len[r]);
+    if (bucket > 0 && (output_len[r] - 1) / bucket >= levels)
+      return fail(SAGE_EINVAL, "request %d (O=%d) needs %d levels, %d given", r, output_len[r],
+                  (output_len[r] - 1) / bucket + 1, levels);
+  }
+  const size_t n = (size_t)levels * R;
+  std::vector<unsigned char> seen(n, 0);
+  for (size_t i = 0; i < n; ++i) {
+    const int32_t e = order[i];
+    if (e < 0 || (size_t)e >= n || seen[e]) return fail(SAGE_EINVAL, "order is not a permutation (at %zu)", i);
+    seen[e] = 1;
+  }
+  if (sage::simulate_queue(arrival, prompt_len, output_len, R, order, levels, informed, bucket, servers,
+                           rate, queue_cap, finish, preemptions) != 0)
+    return fail(SAGE_EINVAL, "sage_simulate: event loop stalled");
+  return ok();
+}

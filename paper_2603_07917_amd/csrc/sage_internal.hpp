@@ -76,4 +76,10 @@ hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, cons
                        int N, float tau, const double* edges, int B, int uniform, int32_t* counts,
                        float* mass, hipStream_t stream);
 
+
+// Host event loop of sage_simulate (inputs already validated); 0 on success.
+int simulate_queue(const double* arrival, const int32_t* prompt_len, const int32_t* output_len, int R,
+                   const int32_t* order, int levels, int informed, int bucket, int servers,
+                   double rate, int queue_cap, double* finish, int32_t* preemptions);
+
 }  // namespace sage

@@ -47,6 +47,7 @@ def load_library():
         "sage_store_insert": (I, [P, P, I, I, ctypes.c_longlong, I, P, P, S]),
         "sage_rank_workspace_bytes": (Z, [I]),
         "sage_rank": (I, [P, I, P, P, Z, S]),
+        "sage_simulate": (I, [P, P, P, I, P, I, I, I, I, ctypes.c_double, I, P, P]),
         "sage_status_string": (ctypes.c_char_p, [I]),
         "sage_last_error": (ctypes.c_char_p, []),
         "sage_timer_create": (I, [I, ctypes.POINTER(P)]),
@@ -267,6 +268,31 @@ def schedule(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tenso
     """Cost -> index -> rank: returns (index, order)."""
     g = index(mass, prompt_len, bin_repr)
     return g, rank(g)
+
+
+def simulate(arrival, prompt_len, output_len, order, *, rate: float, servers: int = 1,
+             queue_cap: int = 1000, bucket: int = 0, levels: int = 1, informed: Optional[int] = None):
+    """Replay a request trace against a queue served in `order` (host-side
+    sage_simulate). Arguments are host arrays; `informed` (default: all) is
+    the number of leading order positions whose entries carry information.
+    Returns (finish [R] float64, preemptions [R] int32) as NumPy arrays."""
+    import numpy as np
+    if any(isinstance(x, torch.Tensor) and x.is_cuda for x in (arrival, prompt_len, output_len, order)):
+        raise SageError("simulate takes host arrays")
+    a = np.ascontiguousarray(arrival, dtype=np.float64)
+    I = np.ascontiguousarray(prompt_len, dtype=np.int32)
+    O = np.ascontiguousarray(output_len, dtype=np.int32)
+    o = np.ascontiguousarray(order, dtype=np.int32)
+    R = a.shape[0]
+    if I.shape != (R,) or O.shape != (R,) or o.shape != (int(levels) * R,):
+        raise SageError("arrival / prompt_len / output_len / order shapes do not match")
+    finish = np.empty(R, dtype=np.float64)
+    pre = np.empty(R, dtype=np.int32)
+    n_inf = int(levels) * R if informed is None else int(informed)
+    _check(load_library().sage_simulate(a.ctypes.data, I.ctypes.data, O.ctypes.data, R, o.ctypes.data,
+                                        int(levels), n_inf, int(bucket), int(servers), float(rate),
+                                        int(queue_cap), finish.ctypes.data, pre.ctypes.data))
+    return finish, pre
 
 
 class Store:

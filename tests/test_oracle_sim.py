@@ -44,6 +44,22 @@ def test_hand_refresh_at_boundaries():
     assert f.tolist() == [10.0, 4.0] and p.tolist() == [2, 1]
 
 
+def test_hand_uninformed_refresh_keeps_the_key():
+    # A: I=0, O=3 (C=4.5, boundaries at a=0.5 and 2); B: I=0, O=1 at t=1 (C=0.5).
+    # Entries e = k*2 + r, order A0 < B0 < A1 < B1 < A2 < B2.
+    order = [0, 1, 2, 3, 4, 5]
+    arr, I, O = [0.0, 1.0], [0, 0], [3, 1]
+    # Every entry informed: A refreshes to A1 at t=0.5, B0 outranks it at t=1 (A stops
+    # with 1.0); B runs 1-1.5; A resumes, reaches level 2 at 2.5 and finishes at 5.
+    f, p = oracle.simulate(arr, I, O, order, servers=1, rate=1.0, queue_cap=4, bucket=1, levels=3)
+    assert f.tolist() == [5.0, 1.5] and p.tolist() == [1, 0]
+    # Only the first two positions informed: A's refreshes carry no information, so A
+    # keeps A0, which outranks B0; A runs to 4.5, then B.
+    f, p = oracle.simulate(arr, I, O, order, servers=1, rate=1.0, queue_cap=4, bucket=1, levels=3,
+                           informed=2)
+    assert f.tolist() == [4.5, 5.0] and p.tolist() == [0, 0]
+
+
 def test_hand_two_servers():
     # rate 2; A (C=8) at 0, B (C=4) at 1, C (C=1.5) at 2; C outranks B outranks A.
     # A runs 0-2 (4 units) and is preempted by C; C runs 2-2.75, A resumes 2.75-4.75;
@@ -244,14 +260,17 @@ def _binned_law_trace(R, seed, B=64, L_max=2048):
 def test_policy_orders():
     mass, I, O, repr_ = _binned_law_trace(300, 9)
     arrival = np.sort(np.random.default_rng(10).random(300)) * 40
-    o_f, L = sage_sim.policy_order("fcfs", arrival, mass, I, repr_)
-    assert L == 1 and np.array_equal(o_f, np.arange(300))
+    o_f, L, n = sage_sim.policy_order("fcfs", arrival, mass, I, repr_)
+    assert L == 1 and n == 300 and np.array_equal(o_f, np.arange(300))
     x = oracle.cost(I, repr_)
-    o_m, _ = sage_sim.policy_order("mean", arrival, mass, I, repr_)
+    o_m, _, _ = sage_sim.policy_order("mean", arrival, mass, I, repr_)
     assert np.array_equal(o_m, np.argsort((mass * x).sum(1).astype(np.float32), kind="stable"))
-    o_s, _ = sage_sim.policy_order("gittins-static", arrival, mass, I, repr_)
-    o_g, L = sage_sim.policy_order("gittins", arrival, mass, I, repr_, O, bucket=64)
+    o_s, _, _ = sage_sim.policy_order("gittins-static", arrival, mass, I, repr_)
+    o_g, L, n = sage_sim.policy_order("gittins", arrival, mass, I, repr_, O, bucket=64)
     assert L == sage_sim.refresh_levels(O, 64) > 1
+    # the uninformed entries are the table's +inf values (no mass above the attained
+    # service): those past the largest representative length, and they rank last
+    assert 300 < n < L * 300
     # level 0 of the refresh table is the index at arrival
     lvl0 = o_g[o_g < 300]
     assert np.array_equal(lvl0, o_s)
