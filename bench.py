@@ -33,8 +33,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
-                    help="workload: 1 tiny, 2 mid (default), 3 gemm-bound, 4 index-bound, 5 streaming")
+    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4", "5", "ttlt"],
+                    help="workload: 1 tiny, 2 mid (default), 3 gemm-bound, 4 index-bound, 5 streaming, "
+                         "ttlt (a Poisson request trace replayed under FCFS / Mean / Gittins)")
+    ap.add_argument("--nodes", type=int, default=64, help="ttlt: servers (8 requests/s each)")
+    ap.add_argument("--requests", type=int, default=32768, help="ttlt: requests in the trace")
+    ap.add_argument("--load", type=float, default=0.9, help="ttlt: offered load per server")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -108,6 +112,9 @@ def main():
     from paper_2603_07917_amd import sage, workloads
 
     torch.cuda.set_device(0)
+    if args.config == "ttlt":
+        return run_ttlt(args, torch, sage, workloads)
+    args.config = int(args.config)
     if args.config == 5:
         return run_streaming(args, torch, sage, workloads)
     if args.config == 4:
@@ -359,6 +366,145 @@ def run_streaming(args, torch, sage, workloads):
                      "traffic": None, "avg_launch_us": k1_avg_s * 1e6, "bytes_per_launch": k1_bytes},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
     }
+    print(json.dumps(line), flush=True)
+
+
+def run_ttlt(args, torch, sage, workloads):
+    """A Poisson request trace over the mid workload's history store, replayed
+    under each queue order. A step is the trace's whole GPU pass: predict
+    every request, then each policy's index values (the refreshed Gittins
+    table: one attained-service launch per bucket level) and their rank. The
+    host replay (sage_simulate) is timed apart."""
+    from paper_2603_07917_amd import simulator
+
+    def log(msg):
+        print(f"# {msg}", file=sys.stderr, flush=True)
+    spec = workloads.CONFIGS[2]
+    R, nodes, bucket, cap = args.requests, args.nodes, 200, 1000
+    rps = 8.0 * nodes
+    log("generating the store and the trace")
+    w = workloads.make_config(2)
+    tr = workloads.make_trace(spec, 2, R, rps)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr), spec.k,
+                       spec.tau)
+    queries, plen = dev(tr.queries), dev(tr.prompt_len)
+    rate = simulator.rate_for_load(tr.prompt_len, tr.output_len, rps, nodes, args.load)
+    chunk = 16384
+    B = spec.B
+    mass = torch.empty((R, B), dtype=torch.float32, device="cuda")
+    n = min(R, chunk)
+    pred_out = (torch.empty((n, spec.k), dtype=torch.int32, device="cuda"),
+                torch.empty((n, spec.k), dtype=torch.float32, device="cuda"),
+                torch.empty((n, B), dtype=torch.int32, device="cuda"))
+    L = simulator.refresh_levels(tr.output_len, bucket)
+    table = torch.empty((L, R), dtype=torch.float32, device="cuda")
+    gen = torch.empty((L, R), dtype=torch.int32, device="cuda")
+    for lv in range(L):
+        gen[lv].fill_(lv * bucket)
+    g_static = torch.empty(R, dtype=torch.float32, device="cuda")
+    g_mean = torch.empty(R, dtype=torch.float32, device="cuda")
+    arr32 = dev(tr.arrival.astype(np.float32))
+    orders = {"fcfs": torch.empty(R, dtype=torch.int32, device="cuda"),
+              "mean": torch.empty(R, dtype=torch.int32, device="cuda"),
+              "gittins-static": torch.empty(R, dtype=torch.int32, device="cuda"),
+              "gittins": torch.empty(L * R, dtype=torch.int32, device="cuda")}
+    rws = torch.empty(max(16, sage.rank_workspace_bytes(L * R)), dtype=torch.uint8, device="cuda")
+
+    def step():
+        for s in range(0, R, chunk):
+            e = min(R, s + chunk)
+            store.predict(queries[s:e], out=tuple(t[:e - s] for t in pred_out) + (mass[s:e],))
+        sage.rank(arr32, workspace=rws, out=orders["fcfs"])
+        sage.index_variant(mass, plen, store.bin_repr, kind="mean", out=g_mean)
+        sage.rank(g_mean, workspace=rws, out=orders["mean"])
+        sage.index(mass, plen, store.bin_repr, out=g_static)
+        sage.rank(g_static, workspace=rws, out=orders["gittins-static"])
+        for lv in range(L):
+            sage.index_attained(mass, plen, store.bin_repr, gen[lv], bucket, out=table[lv])
+        sage.rank(table.view(-1), workspace=rws, out=orders["gittins"])
+
+    log("warmup")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("timed passes")
+    timer = sage.StageTimer(capacity=(L + 64) * (args.steps + 1))
+    with timer:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    stages = timer.totals()
+    timer.close()
+
+    log("replaying the trace")
+    informed = int(np.isfinite(table.cpu().numpy()).sum())
+    host_orders = {pol: o.cpu().numpy() for pol, o in orders.items()}
+
+    def replay(arrival, servers, rate_s):
+        out = {}
+        for pol, o in host_orders.items():
+            t1 = time.perf_counter()
+            refresh = pol == "gittins"
+            finish, pre = sage.simulate(arrival, tr.prompt_len, tr.output_len, o, rate=rate_s,
+                                        servers=servers, queue_cap=cap, bucket=bucket if refresh else 0,
+                                        levels=L if refresh else 1, informed=informed if refresh else None)
+            T = finish - arrival
+            out[pol] = {"mean_ttlt_s": float(T.mean()), "p99_ttlt_s": float(np.percentile(T, 99)),
+                        "preemptions": int(pre.sum()), "replay_ms": 1e3 * (time.perf_counter() - t1)}
+        base = out["gittins"]["mean_ttlt_s"]
+        for pol in out:
+            out[pol]["gittins_reduction"] = 1.0 - base / out[pol]["mean_ttlt_s"]
+        return out
+
+    policies = replay(tr.arrival, nodes, rate)
+    # the same requests on one server at 8 requests/s (arrival times stretched by the
+    # number of servers; the queue orders do not depend on the arrival times)
+    rate1 = simulator.rate_for_load(tr.prompt_len, tr.output_len, 8.0, 1, args.load)
+    single = replay(tr.arrival * nodes, 1, rate1)
+
+    n_launch, k1_ms = stages["sim_topk"]
+    k1_avg_s = k1_ms / n_launch / 1e3
+    rows = R / n_launch * args.steps                 # queries per predict launch (chunked)
+    flops = 2.0 * rows * spec.N * spec.d
+    achieved = flops / k1_avg_s / 1e12
+    line = {
+        "metric": "scheduling decisions/sec (predict+cost+index+rank)",
+        "value": R * args.steps / elapsed,
+        "unit": "decisions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"ttlt: {R}-request Poisson trace at 8 req/s x {nodes} servers over "
+                               f"the mid store (N={spec.N} d={spec.d} k={spec.k} B={spec.B}), "
+                               f"load {args.load}, <= {cap} queued, bucket {bucket}",
+                   "R": R, "servers": nodes, "rps": rps, "load": args.load, "queue_cap": cap,
+                   "bucket": bucket, "levels": L, "rate_cost_per_s": rate, "seed": [workloads.SEED_BASE, 2]},
+        "policies": policies,
+        "single_server": {"rps": 8.0, "rate_cost_per_s": rate1, "policies": single},
+        "gpu_us_per_request": 1e6 * elapsed / args.steps / R,
+        "roofline": {"bound": "mfma", "kernel": kernel_name(spec.k), "achieved": achieved,
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                     "avg_launch_us": k1_avg_s * 1e6, "flops_per_launch": flops},
+        "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
+    }
+    if not args.no_cpu_baseline:
+        import copy
+        ws = copy.copy(w)
+        ws.queries, ws.prompt_len = tr.queries, tr.prompt_len
+        ws.spec = copy.copy(spec)
+        ws.spec.Q = R
+        line["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 
