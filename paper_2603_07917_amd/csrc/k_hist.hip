@@ -11,8 +11,8 @@ namespace {
 // a sum of up to 256 of them below 2^63. Integer sums are order independent.
 constexpr double kWeightScale = 8796093022208.0;  // 2^43
 
-// Largest b in [0, B-1] with edges[b] <= L (0 when L < edges[0]).
-__device__ __forceinline__ int length_bin(const double* __restrict__ edges, int B, int L) {
+// Largest b in [0, B-1] with edges[b] <= L (0 when L < edges[0]); edges in LDS.
+__device__ __forceinline__ int length_bin(const double* edges, int B, int L) {
   const double x = (double)L;
   int lo = 0, hi = B;   // invariant: edges[lo] <= x or lo == 0; the answer is < hi
   while (hi - lo > 1) {
@@ -22,43 +22,67 @@ __device__ __forceinline__ int length_bin(const double* __restrict__ edges, int 
   return lo;
 }
 
-// One wavefront per request; QPB requests per workgroup share nothing but
-// the launch. LDS per wave: B int32 counts + B uint64 fixed-point weights.
-// A neighbour at or above tau weighs its similarity, or 1 when `uniform`
-// (the paper's unweighted form).
-template <int QPB>
-__global__ void __launch_bounds__(64 * QPB) hist_kernel(
+constexpr int kMaxNbr = 256;   // SAGE_MAX_K
+
+// WPR wavefronts per request and QPB requests per workgroup. LDS: the bin
+// edges when kEdgesLds (shared by the workgroup; otherwise they are read from
+// global memory through L1), then per request B uint64 fixed-point weights,
+// B int32 counts and the request's totals. A neighbour at or above tau weighs
+// its similarity, or 1 when `uniform` (the paper's unweighted form). With kVec
+// (B % 4 == 0) each thread writes 4 consecutive bins with 16-byte stores.
+template <int QPB, int WPR, bool kVec, bool kEdgesLds>
+__global__ void __launch_bounds__(64 * QPB * WPR) hist_kernel(
     const int32_t* __restrict__ ids, const float* __restrict__ sims, int Q, int k,
     const int32_t* __restrict__ hist_len, int N, float tau, const double* __restrict__ edges, int B,
     int uniform, int32_t* __restrict__ counts, float* __restrict__ mass) {
+  constexpr int kThreads = kWave * WPR;             // threads per request
+  constexpr int kPer = kMaxNbr / kThreads;          // neighbours per thread at most
   extern __shared__ __align__(16) unsigned char smem[];
-  const int w = threadIdx.x / kWave;
-  const int lane = (int)lane_id();
-  uint64_t* wsum = reinterpret_cast<uint64_t*>(smem) + (size_t)w * B;
-  uint32_t* cnt = reinterpret_cast<uint32_t*>(reinterpret_cast<uint64_t*>(smem) + (size_t)QPB * B) +
-                  (size_t)w * B;
-  const int q = blockIdx.x * QPB + w;
+  const int r = threadIdx.x / kThreads;             // request within the workgroup
+  const int t = threadIdx.x % kThreads;
+  // LDS layout (8-byte words): edges [n_edges] | totals [QPB][2] | weights [QPB][B] | counts
+  const int n_edges = kEdgesLds ? (B + 2) & ~1 : 0;  // B + 1 edges, padded to 16 bytes
+  double* edges_s = reinterpret_cast<double*>(smem);
+  uint64_t* tot = reinterpret_cast<uint64_t*>(smem) + n_edges + 2 * r;           // wtot, m
+  uint64_t* wsum = reinterpret_cast<uint64_t*>(smem) + n_edges + 2 * QPB + (size_t)r * B;
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(reinterpret_cast<uint64_t*>(smem) + n_edges + 2 * QPB +
+                                               (size_t)QPB * B) + (size_t)r * B;
+  const double* edge = kEdgesLds ? edges_s : edges;
+  const int q = blockIdx.x * QPB + r;
   const bool active = q < Q;
 
-  for (int b = lane; b < B; b += kWave) { cnt[b] = 0u; wsum[b] = 0ull; }
+  // Neighbour lists first, so that their latency overlaps the LDS set-up.
+  int32_t id[kPer];
+  float sim[kPer];
+  const size_t row = (size_t)q * (size_t)k;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = t + j * kThreads;
+    const bool in = active && i < k;
+    id[j] = in ? ids[row + i] : -1;
+    sim[j] = in ? sims[row + i] : 0.0f;
+  }
+  if (kEdgesLds)
+    for (int i = threadIdx.x; i <= B; i += blockDim.x) edges_s[i] = edges[i];
+  for (int b = t; b < B; b += kThreads) { cnt[b] = 0u; wsum[b] = 0ull; }
+  if (t < 2) tot[t] = 0ull;
+  int32_t len[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) len[j] = (id[j] >= 0 && id[j] < N) ? hist_len[id[j]] : 0;
   __syncthreads();
 
   uint64_t wtot = 0;
   int m = 0;
-  if (active) {
-    const size_t row = (size_t)q * (size_t)k;
-    for (int i = lane; i < k; i += kWave) {
-      const int32_t id = ids[row + i];
-      if (id < 0 || id >= N) continue;
-      const int b = length_bin(edges, B, hist_len[id]);
-      atomicAdd(&cnt[b], 1u);
-      ++m;
-      const float s = sims[row + i];
-      if (s >= tau) {
-        const uint64_t fx = (uint64_t)((uniform ? 1.0 : (double)s) * kWeightScale);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&wsum[b]), (unsigned long long)fx);
-        wtot += fx;
-      }
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    if (id[j] < 0 || id[j] >= N) continue;
+    const int b = length_bin(edge, B, len[j]);
+    atomicAdd(&cnt[b], 1u);
+    ++m;
+    if (sim[j] >= tau) {
+      const uint64_t fx = (uint64_t)((uniform ? 1.0 : (double)sim[j]) * kWeightScale);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&wsum[b]), (unsigned long long)fx);
+      wtot += fx;
     }
   }
 #pragma unroll
@@ -66,17 +90,37 @@ __global__ void __launch_bounds__(64 * QPB) hist_kernel(
     wtot += (uint64_t)__shfl_xor((unsigned long long)wtot, off, kWave);
     m += __shfl_xor(m, off, kWave);
   }
+  if (WPR > 1 && (t % kWave) == 0) {
+    atomicAdd(reinterpret_cast<unsigned long long*>(&tot[0]), (unsigned long long)wtot);
+    atomicAdd(reinterpret_cast<unsigned long long*>(&tot[1]), (unsigned long long)m);
+  }
   __syncthreads();
   if (!active) return;
+  if (WPR > 1) {
+    wtot = tot[0];
+    m = (int)tot[1];
+  }
   const size_t out = (size_t)q * (size_t)B;
-  const double inv_m = m > 0 ? 1.0 / (double)m : 0.0;
-  for (int b = lane; b < B; b += kWave) {
-    const uint32_t c = cnt[b];
-    counts[out + b] = (int32_t)c;
-    float v;
-    if (wtot > 0) v = (float)((double)wsum[b] / (double)wtot);
-    else v = (float)((double)c * inv_m);
-    mass[out + b] = v;
+  const bool weighted = wtot > 0;
+  const double scale = weighted ? 1.0 / (double)wtot : (m > 0 ? 1.0 / (double)m : 0.0);
+  auto share = [&](uint32_t c, uint64_t ws) -> float {
+    return (float)((weighted ? (double)ws : (double)c) * scale);
+  };
+  if (kVec) {
+    for (int b = t * 4; b < B; b += 4 * kThreads) {
+      const uint4 c = *reinterpret_cast<const uint4*>(cnt + b);
+      const ulonglong2 s01 = *reinterpret_cast<const ulonglong2*>(wsum + b);
+      const ulonglong2 s23 = *reinterpret_cast<const ulonglong2*>(wsum + b + 2);
+      *reinterpret_cast<int4*>(counts + out + b) = make_int4((int)c.x, (int)c.y, (int)c.z, (int)c.w);
+      *reinterpret_cast<float4*>(mass + out + b) =
+          make_float4(share(c.x, s01.x), share(c.y, s01.y), share(c.z, s23.x), share(c.w, s23.y));
+    }
+  } else {
+    for (int b = t; b < B; b += kThreads) {
+      const uint32_t c = cnt[b];
+      counts[out + b] = (int32_t)c;
+      mass[out + b] = share(c, wsum[b]);
+    }
   }
 }
 
@@ -86,17 +130,21 @@ hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, cons
                        int N, float tau, const double* edges, int B, int uniform, int32_t* counts,
                        float* mass, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
+  if (k > kMaxNbr) return hipErrorInvalidValue;
   LaunchScope scope("hist", stream);
-  if (B <= 1024) {
-    constexpr int qpb = 4;
-    const size_t lds = (size_t)qpb * B * 12;
-    hipLaunchKernelGGL(hist_kernel<qpb>, dim3((Q + qpb - 1) / qpb), dim3(64 * qpb), lds, stream, ids,
-                       sims, Q, k, hist_len, N, tau, edges, B, uniform, counts, mass);
-  } else {
-    const size_t lds = (size_t)B * 12;
-    hipLaunchKernelGGL(hist_kernel<1>, dim3(Q), dim3(64), lds, stream, ids, sims, Q, k, hist_len,
-                       N, tau, edges, B, uniform, counts, mass);
+  const bool vec = B % 4 == 0;
+  // LDS bytes: edges (when staged) + per request 12 B per bin + 16 B of totals
+#define SAGE_HIST_LAUNCH(QPB, WPR, VEC, ELDS)                                                        \
+  hipLaunchKernelGGL((hist_kernel<QPB, WPR, VEC, ELDS>), dim3((Q + QPB - 1) / QPB),                 \
+                     dim3(64 * QPB * WPR),                                                           \
+                     (ELDS ? (size_t)((B + 2) & ~1) * 8 : 0) + (size_t)QPB * (B * 12 + 16), stream,  \
+                     ids, sims, Q, k, hist_len, N, tau, edges, B, uniform, counts, mass)
+  if (B <= 1024) {               // one wave per request, edges in LDS
+    if (vec) SAGE_HIST_LAUNCH(4, 1, true, true); else SAGE_HIST_LAUNCH(4, 1, false, true);
+  } else {                       // four waves per request, edges through L1
+    if (vec) SAGE_HIST_LAUNCH(1, 4, true, false); else SAGE_HIST_LAUNCH(1, 4, false, false);
   }
+#undef SAGE_HIST_LAUNCH
   return hipGetLastError();
 }
 
