@@ -40,7 +40,9 @@ enum IndexMode { kGivenCost = 0, kFused = 1, kAttained = 2, kVariant = 3 };
 // Workgroups per CU the register budget is tuned for (4 waves each).
 template <int C> struct IndexOcc { static constexpr int value = C <= 8 ? 4 : (C == 16 ? 3 : 1); };
 
-template <int C, bool kFull, int kMode>
+constexpr int kNoBin = 0x7fffffff;   // a lane without a candidate bin
+
+template <int C, bool kFull, int kMode, bool kArg>
 __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const float* __restrict__ mass,
                                                     const float* __restrict__ cost,
                                                     const int32_t* __restrict__ prompt_len,
@@ -123,16 +125,17 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
       const double s_incl = s_base + lane_s;
       if (lane == kWave - 1) {
         index[q] = f_total > 0.0 ? (float)(s_incl / f_total) : __builtin_inff();
-        if (argmin) argmin[q] = -1;
+        if (kArg) argmin[q] = -1;
       }
       continue;
     }
 
     // Branch-free running minimum of n / f by cross-multiplication; the
-    // start values (n, f) = (1, 0) lose to the first bin with f > 0, and a
-    // later bin must be strictly smaller to win (ties keep the lower bin).
+    // start values (n, f) = (1, 0) lose to the first bin with f > 0 (f never
+    // decreases, so no bin with f = 0 can win later), and a later bin must be
+    // strictly smaller to win (ties keep the lower bin).
     double best_n = 1.0, best_f = 0.0;
-    int best_b = -1;
+    int best_b = kNoBin;
     double f_run = f_base, s_run = s_base, t_run = f_total - f_base;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
@@ -142,35 +145,44 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
       s_run = fma(pj, xj, s_run);
       t_run -= pj;                                  // mass strictly above bin j
       const double n = fma(t_run, xj, s_run);
-      const bool take = (kFull || b0 + j < B) && f_run > 0.0 && n * best_f < best_n * f_run;
+      const bool take = (kFull || b0 + j < B) && n * best_f < best_n * f_run;
       best_n = take ? n : best_n;
       best_f = take ? f_run : best_f;
-      best_b = take ? b0 + j : best_b;
+      if (kArg) best_b = take ? b0 + j : best_b;
     }
-    // Wave-wide minimum of n/f, ties keeping the smaller bin: butterflies
-    // within rows of 16 (quads, half rows, rows), then rows 0+1 -> 1, 2+3 -> 3
-    // and 1 -> 3; lane 63 ends with the row's result. The combine is
-    // idempotent, so lanes left out of a step simply combine with themselves.
-    auto combine = [&](double on, double of, int ob) {
-      const double lhs = on * best_f, rhs = best_n * of;
-      const bool take = ob >= 0 && (best_b < 0 || lhs < rhs || (lhs == rhs && ob < best_b));
-      best_n = take ? on : best_n;
-      best_f = take ? of : best_f;
-      best_b = take ? ob : best_b;
-    };
-#define SAGE_ARGMIN_STEP(CTRL, ROWS)                                                      \
-    combine(dpp_f64<CTRL, ROWS>(best_n, best_n), dpp_f64<CTRL, ROWS>(best_f, best_f),     \
-            (int)dpp_u32<CTRL, ROWS>((uint32_t)best_b, (uint32_t)best_b))
-    SAGE_ARGMIN_STEP(kDppQuadXor1, 0xf);
-    SAGE_ARGMIN_STEP(kDppQuadXor2, 0xf);
-    SAGE_ARGMIN_STEP(kDppRowHalfMirror, 0xf);
-    SAGE_ARGMIN_STEP(kDppRowMirror, 0xf);
-    SAGE_ARGMIN_STEP(kDppRowBcast15, 0xa);
-    SAGE_ARGMIN_STEP(kDppRowBcast31, 0xc);
+    // One division per lane, then the wave-wide minimum of the ratios
+    // (ties keep the smaller bin when the argmin is wanted): butterflies within
+    // rows of 16 (quads, half rows, rows), then rows 0+1 -> 1, 2+3 -> 3 and
+    // 1 -> 3; lane 63 ends with the row's result. Lanes without a candidate
+    // carry +inf and lose every tie.
+    double r = best_f > 0.0 ? best_n / best_f : __builtin_inf();
+    if (kArg) {
+      auto combine = [&](double orr, int ob) {
+        const bool take = orr < r || (orr == r && ob < best_b);
+        r = take ? orr : r;
+        best_b = take ? ob : best_b;
+      };
+#define SAGE_ARGMIN_STEP(CTRL, ROWS) \
+      combine(dpp_f64<CTRL, ROWS>(r, r), (int)dpp_u32<CTRL, ROWS>((uint32_t)best_b, (uint32_t)best_b))
+      SAGE_ARGMIN_STEP(kDppQuadXor1, 0xf);
+      SAGE_ARGMIN_STEP(kDppQuadXor2, 0xf);
+      SAGE_ARGMIN_STEP(kDppRowHalfMirror, 0xf);
+      SAGE_ARGMIN_STEP(kDppRowMirror, 0xf);
+      SAGE_ARGMIN_STEP(kDppRowBcast15, 0xa);
+      SAGE_ARGMIN_STEP(kDppRowBcast31, 0xc);
 #undef SAGE_ARGMIN_STEP
+    } else {
+      r = fmin(r, dpp_f64<kDppQuadXor1, 0xf>(r, r));
+      r = fmin(r, dpp_f64<kDppQuadXor2, 0xf>(r, r));
+      r = fmin(r, dpp_f64<kDppRowHalfMirror, 0xf>(r, r));
+      r = fmin(r, dpp_f64<kDppRowMirror, 0xf>(r, r));
+      r = fmin(r, dpp_f64<kDppRowBcast15, 0xa>(r, r));
+      r = fmin(r, dpp_f64<kDppRowBcast31, 0xc>(r, r));
+    }
     if (lane == kWave - 1) {
-      index[q] = best_b >= 0 ? (float)(best_n / best_f) : __builtin_inff();
-      if (argmin) argmin[q] = best_b;
+      const bool found = r < __builtin_inf();
+      index[q] = found ? (float)r : __builtin_inff();
+      if (kArg) argmin[q] = found ? best_b : -1;
     }
   }
 }
@@ -186,8 +198,14 @@ hipError_t launch_index_v(const float* mass, const float* cost, const int32_t* p
   if (blocks > 65535) blocks = 65535;
   if (blocks < 1) blocks = 1;
   const size_t lds = kMode != kGivenCost ? (size_t)B * sizeof(double) : 0;   // representatives
-  hipLaunchKernelGGL((index_kernel<C, kFull, kMode>), dim3((unsigned)blocks), dim3(64 * waves_per_block),
-                     lds, stream, mass, cost, prompt_len, repr, generated, bucket, Q, B, index, argmin, var);
+  if (argmin)
+    hipLaunchKernelGGL((index_kernel<C, kFull, kMode, true>), dim3((unsigned)blocks),
+                       dim3(64 * waves_per_block), lds, stream, mass, cost, prompt_len, repr, generated,
+                       bucket, Q, B, index, argmin, var);
+  else
+    hipLaunchKernelGGL((index_kernel<C, kFull, kMode, false>), dim3((unsigned)blocks),
+                       dim3(64 * waves_per_block), lds, stream, mass, cost, prompt_len, repr, generated,
+                       bucket, Q, B, index, argmin, var);
   return hipGetLastError();
 }
 
