@@ -73,6 +73,26 @@ def read_traffic(kernel: str, workload_key: str):
         return None
 
 
+def stage_rooflines(stages, rows_per_launch: float, d: int, k: int, B: int):
+    """The HBM-bound stages of the decision: algorithmic bytes per launch
+    (query ingest 6 B per element; histogram Q(12k + 8B): ids, sims and the
+    gathered lengths in, counts and masses out; index Q(4B + 8): masses and
+    prompt lengths in, index out) over the mean launch time from the timer."""
+    per = {"ingest_bf16": 6.0 * rows_per_launch * d,
+           "hist": rows_per_launch * (12.0 * k + 8.0 * B),
+           "index_scan": rows_per_launch * (4.0 * B + 8.0)}
+    out = {}
+    for name, byts in per.items():
+        if name not in stages:
+            continue
+        n, ms = stages[name]
+        us = ms / n * 1e3
+        gbs = byts / us / 1e3
+        out[name] = {"bytes_per_launch": byts, "avg_launch_us": us, "GB_s": gbs,
+                     "frac_of_hbm_peak": gbs / HBM_PEAK_GBS}
+    return out
+
+
 def kernel_name(k: int) -> str:
     """The kernel behind the `sim_topk` timer label: the filtered path for k <= 64."""
     return "sim_filter_kernel" if k <= 64 else "sim_topk_kernel"
@@ -211,6 +231,7 @@ def main():
                      "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
                      "avg_launch_us": k1_avg_s * 1e6, "flops_per_launch": flops},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
+        "stage_rooflines": stage_rooflines(stages, Q, d, k, B),
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
@@ -442,16 +463,23 @@ def run_ttlt(args, torch, sage, workloads):
 
     log("replaying the trace")
     informed = int(np.isfinite(table.cpu().numpy()).sum())
-    host_orders = {pol: o.cpu().numpy() for pol, o in orders.items()}
+    host_orders = {pol: (o.cpu().numpy(), L if pol == "gittins" else 1,
+                         informed if pol == "gittins" else R, pol == "gittins")
+                   for pol, o in orders.items()}
+    # The same policies on inaccurate predictions (Sec. 4.3: a uniform
+    # distribution merged in at 1:4); outside the timed region.
+    for pol in ("mean", "gittins-static", "gittins"):
+        o, lv, inf_n = simulator.policy_order(pol, mass, plen, store.bin_repr, tr.arrival, tr.output_len,
+                                              bucket, noise=0.2)
+        host_orders[pol + "+noise"] = (o.cpu().numpy(), lv, inf_n, pol == "gittins")
 
     def replay(arrival, servers, rate_s):
         out = {}
-        for pol, o in host_orders.items():
+        for pol, (o, lv, inf_n, refresh) in host_orders.items():
             t1 = time.perf_counter()
-            refresh = pol == "gittins"
             finish, pre = sage.simulate(arrival, tr.prompt_len, tr.output_len, o, rate=rate_s,
                                         servers=servers, queue_cap=cap, bucket=bucket if refresh else 0,
-                                        levels=L if refresh else 1, informed=informed if refresh else None)
+                                        levels=lv, informed=inf_n)
             T = finish - arrival
             out[pol] = {"mean_ttlt_s": float(T.mean()), "p99_ttlt_s": float(np.percentile(T, 99)),
                         "preemptions": int(pre.sum()), "replay_ms": 1e3 * (time.perf_counter() - t1)}
@@ -497,6 +525,8 @@ def run_ttlt(args, torch, sage, workloads):
                      "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
                      "avg_launch_us": k1_avg_s * 1e6, "flops_per_launch": flops},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
+        "stage_rooflines": stage_rooflines({n: v for n, v in stages.items() if n != "index_scan"},
+                                           rows, spec.d, spec.k, spec.B),
     }
     if not args.no_cpu_baseline:
         import copy

@@ -213,6 +213,19 @@ int sage_histogram_variant(const int32_t* nbr_ids, const float* nbr_sims, int Q,
  * (+inf for a row with no mass), argmin_bin [Q] int32 out or NULL.
  * SAGE_EINVAL for unknown enums or noise_weight outside [0, 1).
  */
+/*
+ * sage_mix_uniform - a deliberately inaccurate prediction (Sec. 4.3 merges a
+ * uniform distribution into the predicted one at 1:4): each row becomes
+ *   out[q, b] = (1 - weight) * mass[q, b] / sum_b mass[q, b] + weight / B
+ * (fp64, rounded to fp32); weight = 0.2 is the paper's 1:4. A row with no
+ * mass stays zero. Any index entry point can then take `out`.
+ *   mass [Q, B] f32 (non-negative), out [Q, B] f32: the same buffer (in
+ *   place) or one that does not overlap it; weight in [0, 1].
+ * SAGE_EINVAL for a weight outside [0, 1], partial overlap, B outside
+ * [1, SAGE_MAX_BINS], NULL or misaligned pointers.
+ */
+int sage_mix_uniform(const float* mass, int Q, int B, float weight, float* out, sage_stream_t stream);
+
 enum { SAGE_COST_RESOURCE = 0, SAGE_COST_OUTPUT = 1, SAGE_COST_OVERALL = 2 };
 enum { SAGE_INDEX_GITTINS = 0, SAGE_INDEX_MEAN = 1 };
 int sage_index_variant(const float* mass, const int32_t* prompt_len, const double* bin_repr, int Q, int B,

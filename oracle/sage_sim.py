@@ -57,7 +57,8 @@ import math
 
 import numpy as np
 
-from .sage_oracle import attained_service, cost, gittins, gittins_attained, mean_index, rank
+from .sage_oracle import (attained_service, cost, gittins, gittins_attained, mean_index, mix_uniform,
+                          rank)
 
 
 def service_cost(prompt_len, output_len) -> np.ndarray:
@@ -167,7 +168,8 @@ def refresh_levels(output_len, bucket: int) -> int:
     return max(1, int(math.ceil(int(np.max(output_len)) / bucket)))
 
 
-def policy_order(policy: str, arrival, mass, prompt_len, bin_repr, output_len=None, bucket: int = 0):
+def policy_order(policy: str, arrival, mass, prompt_len, bin_repr, output_len=None, bucket: int = 0,
+                 noise: float = 0.0):
     """Queue order of a policy, as (order, levels, informed).
 
     * ``fcfs``: arrival order (vLLM's default, Sec. 2);
@@ -180,11 +182,15 @@ def policy_order(policy: str, arrival, mass, prompt_len, bin_repr, output_len=No
 
     The index values order the queue; the order is taken on their fp32
     values (the precision the scheduling kernels emit), ties to the lower
-    entry id.
+    entry id. With ``noise`` = w > 0 the predicted distributions are first
+    merged with the uniform one at w : (1 - w) (Sec. 4.3's inaccurate
+    predictions, w = 0.2 for 1:4).
     """
     R = len(prompt_len)
     if policy == "fcfs":
         return rank(np.asarray(arrival, dtype=np.float64)), 1, R
+    if noise > 0.0:
+        mass = mix_uniform(mass, noise)
     x = cost(prompt_len, bin_repr)
     if policy == "mean":
         return rank(mean_index(mass, x).astype(np.float32)), 1, R
@@ -201,10 +207,10 @@ def policy_order(policy: str, arrival, mass, prompt_len, bin_repr, output_len=No
 
 
 def simulate_policy(policy: str, arrival, mass, prompt_len, bin_repr, output_len, *, servers: int,
-                    rate: float, queue_cap: int, bucket: int = 200):
+                    rate: float, queue_cap: int, bucket: int = 200, noise: float = 0.0):
     """Order the queue by `policy` and simulate; returns (ttlt, preemptions)."""
     order, levels, informed = policy_order(policy, arrival, mass, prompt_len, bin_repr, output_len,
-                                           bucket)
+                                           bucket, noise)
     b = bucket if policy == "gittins" else 0
     finish, pre = simulate(arrival, prompt_len, output_len, order, servers=servers, rate=rate,
                            queue_cap=queue_cap, bucket=b, levels=levels, informed=informed)

@@ -52,6 +52,27 @@ __global__ void __launch_bounds__(256) store_insert_kernel(const float* __restri
   }
 }
 
+// A deliberately inaccurate prediction: each row merged with the uniform
+// distribution, out = (1 - w) p / sum(p) + w / B in fp64, rounded to fp32; a
+// row with no mass stays zero. One wavefront per row; the row sum is complete
+// before any element is written, so out may alias mass.
+__global__ void __launch_bounds__(256) mix_uniform_kernel(const float* mass, int Q, int B, float w,
+                                                          float* out) {
+  const int lane = (int)lane_id();
+  const int n_waves = (int)(gridDim.x * (blockDim.x / kWave));
+  for (int q = (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave); q < Q; q += n_waves) {
+    const size_t row = (size_t)q * (size_t)B;
+    double sum = 0.0;
+    for (int b = lane; b < B; b += kWave) sum += (double)mass[row + b];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+    const bool empty = !(sum > 0.0);
+    const double keep = empty ? 0.0 : (1.0 - (double)w) / sum;
+    const double spread = empty ? 0.0 : (double)w / (double)B;
+    for (int b = lane; b < B; b += kWave) out[row + b] = (float)fma(keep, (double)mass[row + b], spread);
+  }
+}
+
 // x[q, b] = r_b^2 / 2 + I_q * r_b in fp64, rounded once to fp32.
 __global__ void __launch_bounds__(256) cost_kernel(const int32_t* __restrict__ prompt_len, int Q,
                                                    const double* __restrict__ repr, int B,
@@ -91,6 +112,15 @@ hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, 
   LaunchScope scope("store_insert", stream);
   hipLaunchKernelGGL(store_insert_kernel, dim3(grid_for(work, 256, 8192)), dim3(256), 0, stream, emb, out_len,
                      n, d, first, total, cap, ring_emb, ring_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_mix_uniform(const float* mass, int Q, int B, float weight, float* out,
+                              hipStream_t stream) {
+  if (Q == 0) return hipSuccess;
+  LaunchScope scope("mix_uniform", stream);
+  hipLaunchKernelGGL(mix_uniform_kernel, dim3(grid_for((size_t)Q, 4, 16384)), dim3(256), 0, stream, mass,
+                     Q, B, weight, out);
   return hipGetLastError();
 }
 

@@ -380,6 +380,25 @@ SAGE_API int sage_index_variant(const float* mass, const int32_t* prompt_len, co
                     "index launch");
 }
 
+SAGE_API int sage_mix_uniform(const float* mass, int Q, int B, float weight, float* out,
+                              sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (!(weight >= 0.0f && weight <= 1.0f))
+    return fail(SAGE_EINVAL, "weight=%g outside [0, 1]", (double)weight);
+  if (Q == 0) return ok();
+  if (!mass || !out) return fail(SAGE_EINVAL, "sage_mix_uniform: NULL pointer");
+  if (!aligned16(mass) || !aligned16(out)) return fail(SAGE_EINVAL, "sage_mix_uniform: misaligned pointer");
+  const char* a = reinterpret_cast<const char*>(mass);
+  const char* o = reinterpret_cast<const char*>(out);
+  const size_t bytes = (size_t)Q * (size_t)B * sizeof(float);
+  if (a != o && a < o + bytes && o < a + bytes)
+    return fail(SAGE_EINVAL, "sage_mix_uniform: out overlaps mass without being the same buffer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_mix_uniform(mass, Q, B, weight, out, (hipStream_t)stream), "mix launch");
+}
+
 SAGE_API int sage_index_attained(const float* mass, const int32_t* prompt_len, const double* bin_repr,
                                  const int32_t* generated, int bucket, int Q, int B, float* index,
                                  int32_t* argmin_bin, sage_stream_t stream) {

@@ -49,6 +49,8 @@ hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, 
                                int cap, uint16_t* ring_emb, int32_t* ring_len, hipStream_t stream);
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
                        float* cost, hipStream_t stream);
+hipError_t launch_mix_uniform(const float* mass, int Q, int B, float weight, float* out,
+                              hipStream_t stream);
 // Index variants: cost model (0 resource, 1 output length, 2 input + 2 output),
 // kind (0 Gittins, 1 mean) and a uniform mixing weight in [0, 1).
 struct IndexVariant {

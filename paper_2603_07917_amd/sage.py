@@ -48,6 +48,7 @@ def load_library():
         "sage_rank_workspace_bytes": (Z, [I]),
         "sage_rank": (I, [P, I, P, P, Z, S]),
         "sage_simulate": (I, [P, P, P, I, P, I, I, I, I, ctypes.c_double, I, P, P]),
+        "sage_mix_uniform": (I, [P, I, I, F, P, S]),
         "sage_status_string": (ctypes.c_char_p, [I]),
         "sage_last_error": (ctypes.c_char_p, []),
         "sage_timer_create": (I, [I, ctypes.POINTER(P)]),
@@ -224,6 +225,19 @@ def index_variant(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.
                                              COST_MODELS[cost_model], INDEX_KINDS[kind], float(noise),
                                              _ptr(g), _ptr(arg), _stream()))
     return (g, arg) if with_argmin else g
+
+
+def mix_uniform(mass: torch.Tensor, weight: float = 0.2, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Each row merged with the uniform distribution at weight : (1 - weight)
+    (0.2 is the paper's 1:4 inaccurate prediction); `out` may be `mass`."""
+    _dev(mass, torch.float32, "mass", 2)
+    Q, B = mass.shape
+    res = out if out is not None else torch.empty_like(mass)
+    _dev(res, torch.float32, "out", 2)
+    if tuple(res.shape) != (Q, B):
+        raise SageError("out must have the shape of mass")
+    _check(load_library().sage_mix_uniform(_ptr(mass), Q, B, float(weight), _ptr(res), _stream()))
+    return res
 
 
 def histogram_variant(nbr_ids: torch.Tensor, nbr_sims: torch.Tensor, hist_len: torch.Tensor, tau: float,

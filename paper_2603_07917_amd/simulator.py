@@ -50,15 +50,19 @@ def rate_for_load(prompt_len, output_len, rps: float, servers: int, load: float)
 
 
 def policy_order(policy: str, mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor,
-                 arrival: np.ndarray, output_len: np.ndarray, bucket: int = 200):
+                 arrival: np.ndarray, output_len: np.ndarray, bucket: int = 200, noise: float = 0.0):
     """Order of one policy on the device: returns (order int32 [levels * R], levels,
     informed), informed being the number of finite index values (the +inf
-    entries of exhausted predictions rank last and carry no information)."""
+    entries of exhausted predictions rank last and carry no information).
+    With noise = w > 0 the distributions are first merged with the uniform one
+    at w : (1 - w) (the paper's inaccurate predictions, w = 0.2 for 1:4)."""
     R = mass.shape[0]
     dev = mass.device
     if policy == "fcfs":
         t = torch.from_numpy(np.asarray(arrival, dtype=np.float32)).to(dev)
         return sage.rank(t), 1, R
+    if noise > 0.0:
+        mass = sage.mix_uniform(mass, noise)
     if policy == "mean":
         return sage.rank(sage.index_variant(mass, prompt_len, bin_repr, kind="mean")), 1, R
     if policy == "gittins-static":
@@ -102,7 +106,7 @@ class Comparison:
 
 def compare(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor, arrival, output_len, *,
             rate: float, servers: int = 1, queue_cap: int = 1000, bucket: int = 200,
-            policies=POLICIES) -> Comparison:
+            policies=POLICIES, noise: float = 0.0) -> Comparison:
     """Replay the trace under each policy, given the predicted distributions
     `mass` [R, B] (device) and prompt lengths (device); arrival and the true
     output lengths are host arrays."""
@@ -113,7 +117,7 @@ def compare(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor
     for pol in policies:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        order, L, informed = policy_order(pol, mass, prompt_len, bin_repr, arrival, O, bucket)
+        order, L, informed = policy_order(pol, mass, prompt_len, bin_repr, arrival, O, bucket, noise)
         order = order.cpu().numpy()
         t1 = time.perf_counter()
         finish, pre = sage.simulate(arrival, I_host, O, order, rate=rate, servers=servers,
@@ -126,7 +130,8 @@ def compare(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor
 
 def compare_trace(store: sage.Store, queries: torch.Tensor, prompt_len: torch.Tensor, arrival,
                   output_len, *, rate: float, servers: int = 1, queue_cap: int = 1000,
-                  bucket: int = 200, chunk: int = 16384, policies=POLICIES) -> Comparison:
+                  bucket: int = 200, chunk: int = 16384, policies=POLICIES,
+                  noise: float = 0.0) -> Comparison:
     """Predict every request's distribution on the store, then `compare`."""
     R = queries.shape[0]
     B = store.bin_edges.shape[0] - 1
@@ -144,7 +149,7 @@ def compare_trace(store: sage.Store, queries: torch.Tensor, prompt_len: torch.Te
     torch.cuda.synchronize()
     predict_ms = 1e3 * (time.perf_counter() - t0)
     out = compare(mass, prompt_len, store.bin_repr, arrival, output_len, rate=rate, servers=servers,
-                  queue_cap=queue_cap, bucket=bucket, policies=policies)
+                  queue_cap=queue_cap, bucket=bucket, policies=policies, noise=noise)
     out.predict_ms = predict_ms
     out.mass = mass
     return out

@@ -37,6 +37,7 @@ def lib():
     lib.sage_index_variant.argtypes = [P, P, P, I, I, I, I, F, P, P, P]
     lib.sage_histogram_variant.argtypes = [P, P, I, I, P, I, F, P, I, I, P, P, P]
     lib.sage_store_insert.argtypes = [P, P, I, I, ctypes.c_longlong, I, P, P, P]
+    lib.sage_mix_uniform.argtypes = [P, I, I, F, P, P]
     lib.sage_rank.argtypes = [P, I, P, P, Z, P]
     lib.sage_cost.argtypes = [P, I, P, I, P, P]
     lib.sage_histogram.argtypes = [P, P, I, I, P, I, F, P, I, P, P, P]
@@ -133,6 +134,14 @@ def test_index_rank_cost_hist_validation(lib):
     assert lib.sage_index_variant(A, A, A, 4, 16, 0, 0, -0.1, A, None, None) == SAGE_EINVAL
     assert lib.sage_index_variant(A, None, A, 4, 16, 0, 0, 0.2, A, None, None) == SAGE_EINVAL
     assert lib.sage_index_variant(None, None, None, 0, 16, 1, 1, 0.2, None, None, None) == SAGE_OK
+    # sage_mix_uniform(mass, Q, B, weight, out, stream)
+    assert lib.sage_mix_uniform(A, 4, 16, 1.5, A, None) == SAGE_EINVAL                     # weight
+    assert lib.sage_mix_uniform(A, 4, 16, -0.1, A, None) == SAGE_EINVAL
+    assert lib.sage_mix_uniform(A, 4, 0, 0.2, A, None) == SAGE_EINVAL                      # B
+    assert lib.sage_mix_uniform(A, 4, 16, 0.2, A + 16, None) == SAGE_EINVAL                # overlap
+    assert lib.sage_mix_uniform(A, 4, 16, 0.2, None, None) == SAGE_EINVAL
+    assert lib.sage_mix_uniform(A + 4, 4, 16, 0.2, A + 4096, None) == SAGE_EINVAL          # alignment
+    assert lib.sage_mix_uniform(None, 0, 16, 0.2, None, None) == SAGE_OK
     # sage_histogram_variant(..., weighting, ...)
     assert lib.sage_histogram_variant(A, A, 4, 8, A, 100, 0.8, A, 16, 2, A, A, None) == SAGE_EINVAL
     # sage_store_insert(emb, out_len, n, d, total, capacity, ring_emb, ring_len, stream)

@@ -10,9 +10,10 @@ Checks, in order:
 * each policy's order is a stable sort of its own GPU index values;
 * the replay of the ORACLE's order by sage_simulate equals the oracle's own
   replay bit for bit (the event loop, on real orders);
-* the mean TTLT of each policy agrees with the oracle's within 2% (where an
-  index pair falls within the fp32 rounding the two orders may differ and
-  change later decisions), and both sides rank the policies the same way.
+* the mean TTLT of each policy agrees with the oracle's within 2%, and at
+  least 95% of the requests have bit-identical TTLTs (where an index pair
+  falls within the fp32 rounding the two orders may differ and change later
+  decisions); policies the oracle separates come out in the same order.
 """
 import numpy as np
 import pytest
@@ -35,15 +36,16 @@ def host(t):
     return t.cpu().numpy()
 
 
-CASES = [  # (R, servers, load, queue_cap, bucket)
-    (1200, 1, 0.9, 1000, 200),
-    (1600, 4, 0.95, 40, 100),
+CASES = [  # (R, servers, load, queue_cap, bucket, noise)
+    (1200, 1, 0.9, 1000, 200, 0.0),
+    (1600, 4, 0.95, 40, 100, 0.0),
+    (1200, 1, 0.9, 1000, 200, 0.2),       # the paper's 1:4 inaccurate predictions
 ]
 
 
-@pytest.mark.parametrize("R,servers,load,cap,bucket", CASES)
-def test_ttlt_policies_vs_oracle(R, servers, load, cap, bucket):
-    print(f"case R={R} servers={servers} load={load} cap={cap} bucket={bucket}", flush=True)
+@pytest.mark.parametrize("R,servers,load,cap,bucket,noise", CASES)
+def test_ttlt_policies_vs_oracle(R, servers, load, cap, bucket, noise):
+    print(f"case R={R} servers={servers} load={load} cap={cap} bucket={bucket} noise={noise}", flush=True)
     spec = workloads.PredictSpec(Q=1, N=6000, d=128, clusters=12, mu_range=(3.0, 6.5),
                                  s_range=(0.3, 1.0), L_max=4096, k=32, B=64)
     cid = 500000 + R
@@ -58,7 +60,7 @@ def test_ttlt_policies_vs_oracle(R, servers, load, cap, bucket):
     ids, sims, counts, mass = [host(t) for t in store.predict(dev(tr.queries))]
     cmp = simulator.compare_trace(store, dev(tr.queries), dev(tr.prompt_len), tr.arrival,
                                   tr.output_len, rate=rate, servers=servers, queue_cap=cap,
-                                  bucket=bucket)
+                                  bucket=bucket, noise=noise)
     assert np.array_equal(host(cmp.mass), mass)
 
     # the oracle: its own prediction from the same inputs
@@ -75,18 +77,19 @@ def test_ttlt_policies_vs_oracle(R, servers, load, cap, bucket):
         res = cmp.results[pol]
         # GPU order of this policy: a stable sort of its own index values
         order_g, L, n_g = simulator.policy_order(pol, dev(mass), dev(tr.prompt_len), dev(w.bin_repr),
-                                                 tr.arrival, tr.output_len, bucket)
+                                                 tr.arrival, tr.output_len, bucket, noise)
+        m_pol = dev(mass) if noise == 0.0 or pol == "fcfs" else sage.mix_uniform(dev(mass), noise)
         order_g = host(order_g)
         assert L == res.levels
         if pol == "fcfs":
             assert np.array_equal(order_g, np.arange(R))
         else:
             if pol == "mean":
-                vals = sage.index_variant(dev(mass), dev(tr.prompt_len), dev(w.bin_repr), kind="mean")
+                vals = sage.index_variant(m_pol, dev(tr.prompt_len), dev(w.bin_repr), kind="mean")
             elif pol == "gittins-static":
-                vals = sage.index(dev(mass), dev(tr.prompt_len), dev(w.bin_repr))
+                vals = sage.index(m_pol, dev(tr.prompt_len), dev(w.bin_repr))
             else:
-                vals = torch.stack([sage.index_attained(dev(mass), dev(tr.prompt_len), dev(w.bin_repr),
+                vals = torch.stack([sage.index_attained(m_pol, dev(tr.prompt_len), dev(w.bin_repr),
                                                         dev(np.full(R, k * bucket, np.int32)), bucket)
                                     for k in range(L)]).view(-1)
             vals = host(vals)
@@ -94,7 +97,7 @@ def test_ttlt_policies_vs_oracle(R, servers, load, cap, bucket):
             assert n_g == int(np.isfinite(vals).sum())
         # the oracle's order and replay
         order_o, L_o, n_o = sage_sim.policy_order(pol, tr.arrival, mass_o, tr.prompt_len, w.bin_repr,
-                                                  tr.output_len, bucket)
+                                                  tr.output_len, bucket, noise)
         assert L_o == L
         b = bucket if pol == "gittins" else 0
         f_o, p_o = oracle.simulate(tr.arrival, tr.prompt_len, tr.output_len, order_o, servers=servers,
@@ -107,6 +110,7 @@ def test_ttlt_policies_vs_oracle(R, servers, load, cap, bucket):
         means_o[pol] = T_o.mean()
         same = np.mean(res.ttlt == T_o)
         assert res.mean_ttlt == pytest.approx(means_o[pol], rel=0.02), pol
+        assert same >= 0.95, (pol, same)
         print(f"{pol}: mean TTLT gpu {res.mean_ttlt:.4f} s, oracle {means_o[pol]:.4f} s, "
               f"{100 * same:.1f}% identical, {int(res.preemptions.sum())} preemptions", flush=True)
     # policies the oracle separates by more than 4% come out in the same order

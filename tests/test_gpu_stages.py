@@ -208,6 +208,23 @@ def test_index_variants_vs_oracle(B, model):
         assert np.array_equal(g0.view(np.uint32), g1.view(np.uint32))
 
 
+@pytest.mark.parametrize("B", [1, 7, 256, 4096])
+def test_mix_uniform_vs_oracle(B):
+    rng = np.random.default_rng(B + 5)
+    Q = 333
+    mass = rng.dirichlet(np.full(B, 0.3), size=Q).astype(np.float32) * rng.uniform(0.5, 2.0, (Q, 1)).astype(np.float32)
+    mass[:4] = 0.0                                                 # empty rows stay empty
+    for w in (0.0, 0.2, 1.0):
+        got = host(sage.mix_uniform(dev(mass), w))
+        want = oracle.mix_uniform(mass.astype(np.float64), w)
+        assert np.all(got[:4] == 0.0)
+        err = np.abs(got.astype(np.float64) - want)
+        assert np.all(err <= 2.0 ** -23 * np.abs(want) + 1e-30), (w, err.max())
+        t = dev(mass)
+        sage.mix_uniform(t, w, out=t)                              # in place
+        assert np.array_equal(host(t), got)
+
+
 @pytest.mark.parametrize("k,B,tau", [(32, 128, 0.8), (64, 256, 0.5), (100, 37, 0.8)])
 def test_histogram_unweighted_vs_oracle(k, B, tau):
     rng = np.random.default_rng(k + B)
