@@ -560,14 +560,6 @@ struct Frags {
 // that epilogues copy tiles out one at a time (bounded register use).
 __device__ __forceinline__ void pin(floatx16& x) { asm volatile("" : "+a"(x)); }
 
-__device__ __forceinline__ void mma(floatx16 (&acc)[4][4], const Frags& f) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-      acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[u], f.b[t], acc[u][t], 0, 0, 0);
-}
-
 // Runs steps h0 = h_first + j * h_stride (j < n_steps) of query tile q0 and
 // calls epi(acc, h0, step_end) after each, step_end = min(h_limit, h0 + 256),
 // with acc[u][t][v] = S[h][q] for
@@ -647,6 +639,12 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
 #pragma unroll
     for (int t = 0; t < 4; ++t) f.b[t] = *reinterpret_cast<const bf16x8*>(stage + b_off[kk] + t * 2048);
   };
+  // Piece p of the fragments: A tile p (p < 4) or B tile p - 4.
+  auto read_piece = [&](int g, int kk, int p, Frags& f) {
+    const char* stage = lds + (g % kStages) * kStageBytes;
+    if (p < 4) f.a[p] = *reinterpret_cast<const bf16x8*>(stage + a_off[kk] + p * 2048);
+    else f.b[p - 4] = *reinterpret_cast<const bf16x8*>(stage + b_off[kk] + (p - 4) * 2048);
+  };
 
   __syncthreads();                              // earlier users of the LDS are done
   const int pre = min(kAhead, total);
@@ -659,32 +657,53 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
   for (int step = 0; step < n_steps; ++step) {
     floatx16 acc[4][4];
     // One slice: f0 holds its first 16 columns on entry; on exit f0 holds the
-    // first 16 columns of slice g + 1.
+    // first 16 columns of slice g + 1 (past the last slice those reads fetch
+    // a stale stage, which is never used).
+    //  * The fragment reads are spread over the MFMAs, one after each of the
+    //    first eight of a half, pinned there with scheduling groups: issued
+    //    as one burst next to their consumers, the compiler waits on them and
+    //    the matrix pipe drains (measured: 1.4 PF/s for a burst schedule
+    //    against 2.0 PF/s interleaved, MFMA + LDS only). A read never
+    //    overwrites a fragment that an MFMA still in the pipe reads: the
+    //    previous users of f1 (f0) were issued a half-slice earlier.
+    //  * The eight loads of slice g + kAhead (whose stage was last read in
+    //    slice g - 1) go out four in each half, which keeps the address unit
+    //    evenly busy.
     auto slice = [&](bool first) {
-      read(g, 1, f1);
-      if (first) {
-        const floatx16 zero = {};
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int t = 0; t < 4; ++t)
-            acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[u], f0.b[t], zero, 0, 0, 0);
-      } else {
-        mma(acc, f0);
-      }
-      // Slice g + 1 must have landed; slices up to min(total - 1, g + kAhead - 1) are issued.
-      wait_slices(min(total - 1, g + kAhead - 1) - (g + 1));
-      barrier();                                // also: all waves are done with stage (g - 1) % kStages
-      if (g + 1 < total) read(g + 1, 0, f0);
-      // The loads of slice g + kAhead (if any) go out between the MFMAs.
       const int more = g + kAhead < total;
+      const floatx16 zero = {};
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int j = 0; j < 16; ++j) {
+        const int u = j >> 2, t = j & 3;
+        acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[u], f0.b[t], first ? zero : acc[u][t], 0, 0, 0);
+        if (j < 8) read_piece(g, 1, j, f1);
+        if (t == 3) issue_one(g + kAhead, u, more);
+      }
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[u], f1.b[t], acc[u][t], 0, 0, 0);
-          if ((4 * u + t) % 2 == 1) issue_one(g + kAhead, (4 * u + t) / 2, more);
-        }
+      for (int j = 0; j < 8; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      const int after = (g + 2 < total ? kLoads : 0) + (more ? kLoads / 2 : 0);
+      if (after == 0) wait_loads<0>();
+      else if (after == kLoads / 2) wait_loads<kLoads / 2>();
+      else if (after == kLoads) wait_loads<kLoads>();
+      else wait_loads<kLoads + kLoads / 2>();
+      barrier();
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int u = j >> 2, t = j & 3;
+        acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[u], f1.b[t], acc[u][t], 0, 0, 0);
+        if (j < 8) read_piece(g + 1, 0, j, f0);
+        if (t == 3) issue_one(g + kAhead, kLoads / 2 + u, more);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
       if (more) advance();
       ++g;
     };
@@ -731,17 +750,6 @@ __global__ void __launch_bounds__(kThreads, 1) threshold_sample_ring_kernel(
   ring::sweep(hist, N, s0 * stride, stride, n_steps, N, queries, Q, q0, d, lds, epi);
 }
 
-// acc[u][t][i % 16] for a lane-varying i = 16u + v: a select tree, no
-// dynamic register indexing.
-__device__ __forceinline__ float pick_score(const floatx16 (&acc)[4][4], int t, int i) {
-  float r = 0.0f;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) r = (i == 16 * u + v) ? acc[u][t][v] : r;
-  return r;
-}
-
 // Filter kernel: every score >= theta0[q] is written as a key to the
 // segment [q][chunk][0..seg_cap) (position from an LDS counter); the true
 // count goes to seg_count[q][chunk] even when the segment overflows.
@@ -751,6 +759,10 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
     int seg_cap, uint64_t* __restrict__ seg, int* __restrict__ seg_count) {
   __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
   __shared__ int cnt[ring::kBQ];
+  // Per-lane rows for reading survivors back by a lane-varying index (16
+  // scores each, padded to 80 bytes so that the 16-byte writes of 16 lanes
+  // fall on distinct banks).
+  __shared__ __align__(16) float stage_rows[4][kWave][20];
   int qt, chunk;
   const int b = blockIdx.x;
   if (q_groups > 0) {
@@ -787,6 +799,7 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
   }
   // Score acc[u][t][v] of this lane is row h0 + 128 wh + 4 half + r(i) for
   // bit i = 16 u + v, r(i) = 32 (i / 16) + 8 ((i / 4) % 4) + i % 4.
+  float* row = &stage_rows[w][lane][0];
   auto epi = [&](floatx16 (&acc)[4][4], int h0, int step_end) {
     const int lim = step_end - h0 - 128 * wh - 4 * half;     // r(i) < lim: row inside the step
     const int hl = h0 + 128 * wh + 4 * half;
@@ -812,11 +825,21 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
       const int ql = 128 * wq + 32 * t + l32;
       const int base = atomicAdd(&cnt[ql], __popcll(m));
       uint64_t* dst = seg + ((size_t)(q0 + ql) * n_chunks + chunk) * seg_cap;
-      for (int j = base; m && j < seg_cap; ++j) {
-        const int i = __ffsll((unsigned long long)m) - 1;
-        m &= m - 1;
-        const int h = hl + 32 * (i >> 4) + 8 * ((i >> 2) & 3) + (i & 3);
-        dst[j] = make_key(pick_score(acc, t, i), (uint32_t)h);
+      int j = base;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t bits = (uint32_t)(m >> (16 * u)) & 0xffffu;
+        if (bits == 0) continue;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          *reinterpret_cast<float4*>(row + 4 * c) =
+              make_float4(acc[u][t][4 * c], acc[u][t][4 * c + 1], acc[u][t][4 * c + 2], acc[u][t][4 * c + 3]);
+        while (bits) {
+          const int v = __ffs(bits) - 1;
+          bits &= bits - 1;
+          if (j < seg_cap) dst[j] = make_key(row[v], (uint32_t)(hl + 32 * u + 8 * (v >> 2) + (v & 3)));
+          ++j;
+        }
       }
     }
   };
