@@ -4,8 +4,8 @@
 
 A step is one scheduling decision for a batch of pending requests: bf16
 ingest of the query embeddings, similarity search + top-k + histogram
-(sage_predict), fused cost + Gittins index (sage_index) and the queue
-ranking (sage_rank). Inputs (the history store, the queries, the prompt
+(sage_predict_layout on the panel-major store and queries), fused cost +
+Gittins index (sage_index) and the queue ranking (sage_rank). Inputs (the history store, the queries, the prompt
 lengths) are resident in HBM before the timed region starts. Prints one JSON
 line with the whole-job throughput in decisions per second, the roofline of
 the dominant kernel (HIP events over the timed region) and the CPU oracle
@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PANELS = 1                         # SAGE_LAYOUT_PANELS
 HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
 
 
@@ -153,7 +154,7 @@ def main():
 
     # Resident inputs (untimed): history store ingested to bf16 once.
     hist_f32 = dev(w.hist_emb)
-    hist = sage.ingest_bf16(hist_f32)
+    hist = sage.ingest_bf16(hist_f32, "panels")          # panel-major resident store
     del hist_f32
     hist_len = dev(w.hist_len)
     edges = dev(w.bin_edges)
@@ -162,7 +163,7 @@ def main():
     prompt_len = dev(w.prompt_len)
 
     # Preallocated outputs and workspaces: a step allocates nothing.
-    qb = torch.empty((Q, d), dtype=torch.bfloat16, device="cuda")
+    qb = torch.empty((d // 32, Q, 32), dtype=torch.bfloat16, device="cuda")
     ids = torch.empty((Q, k), dtype=torch.int32, device="cuda")
     sims = torch.empty((Q, k), dtype=torch.float32, device="cuda")
     counts = torch.empty((Q, B), dtype=torch.int32, device="cuda")
@@ -175,11 +176,12 @@ def main():
     stream = torch.cuda.current_stream().cuda_stream
 
     def step():
-        sage._check(lib.sage_ingest_bf16(queries_f32.data_ptr(), Q * d, qb.data_ptr(), stream))
-        sage._check(lib.sage_predict(qb.data_ptr(), Q, hist.data_ptr(), hist_len.data_ptr(), N, d, k,
-                                     float(spec.tau), edges.data_ptr(), B, ids.data_ptr(),
-                                     sims.data_ptr(), counts.data_ptr(), mass.data_ptr(),
-                                     ws.data_ptr(), ws.numel(), stream))
+        sage._check(lib.sage_ingest_bf16_panels(queries_f32.data_ptr(), Q, d, qb.data_ptr(), stream))
+        sage._check(lib.sage_predict_layout(qb.data_ptr(), PANELS, Q, hist.data_ptr(), PANELS,
+                                            hist_len.data_ptr(), N, d, k, float(spec.tau),
+                                            edges.data_ptr(), B, ids.data_ptr(), sims.data_ptr(),
+                                            counts.data_ptr(), mass.data_ptr(), ws.data_ptr(),
+                                            ws.numel(), stream))
         sage._check(lib.sage_index(mass.data_ptr(), None, prompt_len.data_ptr(), repr_.data_ptr(), Q,
                                    B, g.data_ptr(), None, stream))
         sage._check(lib.sage_rank(g.data_ptr(), Q, order.data_ptr(), rws.data_ptr(), rws.numel(),
@@ -224,7 +226,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": workloads.WORKLOAD_NAMES[args.config], "Q": Q, "N": N, "d": d,
-                   "k": k, "B": B, "tau": spec.tau, "seed": w.seed},
+                   "k": k, "B": B, "tau": spec.tau, "layout": "panels", "seed": w.seed},
         "roofline": {"bound": "mfma", "kernel": kernel_name(k), "achieved": achieved,
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,

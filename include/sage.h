@@ -56,6 +56,36 @@ enum sage_status {
 int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_stream_t stream);
 
 /*
+ * Layouts of an embedding matrix of `rows` x d bf16 values (d % 32 == 0).
+ *   SAGE_LAYOUT_ROWS    row-major [rows, d]
+ *   SAGE_LAYOUT_PANELS  panel-major [d / 32][rows][32]: the d axis is cut into
+ *                       32-column panels, each holding its columns of every
+ *                       row contiguously; element (r, c) is at
+ *                       (c / 32) * rows * 32 + r * 32 + c % 32
+ * The similarity kernels walk d in 32-column slices of consecutive rows;
+ * panel-major makes each slice of 16 rows one contiguous kilobyte (whole
+ * 128-byte lines), which halves the L2 requests of the search. Results do not
+ * depend on the layout (bit-identical outputs).
+ */
+enum { SAGE_LAYOUT_ROWS = 0, SAGE_LAYOUT_PANELS = 1 };
+
+/*
+ * sage_ingest_bf16_panels - sage_ingest_bf16 into the panel-major layout.
+ *   src [rows, d] fp32 row-major finite values; dst [d / 32][rows][32] bf16
+ *   bits (round to nearest, ties to even). src and dst must not overlap.
+ * SAGE_EINVAL: rows < 0 or above 2^29, d not a positive multiple of 32, NULL
+ * or misaligned pointer. rows = 0 is a no-op.
+ */
+int sage_ingest_bf16_panels(const float* src, int rows, int d, uint16_t* dst, sage_stream_t stream);
+
+/*
+ * sage_panels_from_rows - rearrange bf16 embeddings [rows, d] (row-major)
+ * into the panel-major layout (bits copied unchanged). Errors as for
+ * sage_ingest_bf16_panels.
+ */
+int sage_panels_from_rows(const uint16_t* src, int rows, int d, uint16_t* dst, sage_stream_t stream);
+
+/*
  * sage_store_insert - FIFO maintenance of the history store (Sec. 3.1: the
  * records of recently served requests, prompt embedding and output length,
  * kept in a window updated first-in first-out). The store is a ring of
@@ -113,6 +143,19 @@ int sage_predict(const uint16_t* queries, int Q,
                  int k, float tau, const double* bin_edges, int B,
                  int32_t* nbr_ids, float* nbr_sims, int32_t* counts, float* mass,
                  void* workspace, size_t workspace_bytes, sage_stream_t stream);
+
+/*
+ * sage_predict_layout - sage_predict with the layout of each embedding
+ * matrix given: queries [Q, d] and hist_emb [N, d] are each SAGE_LAYOUT_ROWS
+ * or SAGE_LAYOUT_PANELS (the panel-major store is the fast one; outputs are
+ * identical). sage_predict is this call with both SAGE_LAYOUT_ROWS.
+ * SAGE_EINVAL also for a layout that is not a SAGE_LAYOUT_* value.
+ */
+int sage_predict_layout(const uint16_t* queries, int query_layout, int Q,
+                        const uint16_t* hist_emb, int hist_layout, const int32_t* hist_len, int N, int d,
+                        int k, float tau, const double* bin_edges, int B,
+                        int32_t* nbr_ids, float* nbr_sims, int32_t* counts, float* mass,
+                        void* workspace, size_t workspace_bytes, sage_stream_t stream);
 
 /*
  * sage_histogram - the predicted output-length distribution alone (the last

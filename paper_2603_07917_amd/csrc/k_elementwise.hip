@@ -28,6 +28,37 @@ __global__ void __launch_bounds__(256) ingest_bf16_kernel(const float* __restric
     dst[i] = bf16_rne(src[i]);
 }
 
+// [rows, d] fp32 -> panel-major bf16 [d / 32][rows][32] (RNE). Block row y
+// walks panels y, y + gridDim.y, ...; a thread writes one 16-byte piece (8
+// values) of a panel row and reads the matching 32 bytes of the source row,
+// so four consecutive threads read one whole 128-byte line.
+__global__ void __launch_bounds__(256) ingest_panels_kernel(const float* __restrict__ src, int rows, int d,
+                                                            uint16_t* __restrict__ dst) {
+  const int pieces = rows * 4;
+  for (int p = blockIdx.y; p < d / 32; p += gridDim.y) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < pieces; i += gridDim.x * blockDim.x) {
+      const float* s = src + (size_t)(i >> 2) * d + p * 32 + (i & 3) * 8;
+      const float4 a = *reinterpret_cast<const float4*>(s);
+      const float4 b = *reinterpret_cast<const float4*>(s + 4);
+      ushort4* out = reinterpret_cast<ushort4*>(dst + ((size_t)p * pieces + i) * 8);
+      out[0] = make_ushort4(bf16_rne(a.x), bf16_rne(a.y), bf16_rne(a.z), bf16_rne(a.w));
+      out[1] = make_ushort4(bf16_rne(b.x), bf16_rne(b.y), bf16_rne(b.z), bf16_rne(b.w));
+    }
+  }
+}
+
+// The same rearrangement of bf16 bits already rounded.
+__global__ void __launch_bounds__(256) panels_from_rows_kernel(const uint16_t* __restrict__ src, int rows,
+                                                               int d, uint16_t* __restrict__ dst) {
+  const int pieces = rows * 4;
+  for (int p = blockIdx.y; p < d / 32; p += gridDim.y) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < pieces; i += gridDim.x * blockDim.x) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)(i >> 2) * d + p * 32 + (i & 3) * 8);
+      *reinterpret_cast<uint4*>(dst + ((size_t)p * pieces + i) * 8) = v;
+    }
+  }
+}
+
 // FIFO insert into the history ring: record i of the batch (only the last
 // `cap` of the batch survive) goes to slot (total + i) mod cap, embedding
 // rounded to bf16 (RNE), length copied. One thread per 8 embedding values.
@@ -101,6 +132,31 @@ hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStre
   LaunchScope scope("ingest_bf16", stream);
   hipLaunchKernelGGL(ingest_bf16_kernel, dim3(grid_for(n / 4 + 1, 256, 8192)), dim3(256), 0, stream,
                      src, n, dst);
+  return hipGetLastError();
+}
+
+namespace {
+dim3 panels_grid(int rows, int d) {
+  const int px = grid_for((size_t)rows * 4, 256, 4096);
+  const int py = d / 32 < 65535 ? d / 32 : 65535;
+  // about 8192 blocks in all
+  int gx = px, gy = py;
+  while ((long)gx * gy > 8192 && gx > 1) gx = (gx + 1) / 2;
+  return dim3(gx, gy);
+}
+}  // namespace
+
+hipError_t launch_ingest_panels(const float* src, int rows, int d, uint16_t* dst, hipStream_t stream) {
+  if (rows == 0) return hipSuccess;
+  LaunchScope scope("ingest_bf16", stream);
+  hipLaunchKernelGGL(ingest_panels_kernel, panels_grid(rows, d), dim3(256), 0, stream, src, rows, d, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_panels_from_rows(const uint16_t* src, int rows, int d, uint16_t* dst, hipStream_t stream) {
+  if (rows == 0) return hipSuccess;
+  LaunchScope scope("panels_from_rows", stream);
+  hipLaunchKernelGGL(panels_from_rows_kernel, panels_grid(rows, d), dim3(256), 0, stream, src, rows, d, dst);
   return hipGetLastError();
 }
 

@@ -33,6 +33,11 @@ namespace sage {
 namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+
+// Address of element (r, c) of an embedding matrix in either layout.
+__device__ __forceinline__ const uint16_t* emb_at(const EmbView& m, int r, int c) {
+  return m.base + (long long)(c >> 5) * m.panel + (long long)r * m.row + (c & 31);
+}
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 
 constexpr int kThreads = 256;
@@ -54,9 +59,8 @@ struct Core {
   // Loads are unconditional (rows clamped into range) so that no branch sits
   // around them; only the zero-fill of columns past d is a select. Rows past
   // h_end and queries past Q carry real but unused data (masked later).
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ hist, int h0, int h_last,
-                                       const uint16_t* __restrict__ queries, int q0, int q_last,
-                                       int d, int kt) {
+  __device__ __forceinline__ void load(const EmbView& hist, int h0, int h_last, const EmbView& queries,
+                                       int q0, int q_last, int d, int kt) {
     const int tid = threadIdx.x;
     const int k0 = kt * kKT;
 #pragma unroll
@@ -64,7 +68,7 @@ struct Core {
       const int f = c * kThreads + tid;
       const int row = f >> 3, col = k0 + (f & 7) * 8;
       const int h = min(h0 + row, h_last);
-      const uint4 v = *reinterpret_cast<const uint4*>(hist + (size_t)h * d + min(col, d - 8));
+      const uint4 v = *reinterpret_cast<const uint4*>(emb_at(hist, h, min(col, d - 8)));
       ra[c] = col < d ? v : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
@@ -72,7 +76,7 @@ struct Core {
       const int f = min(c * kThreads + tid, B_CHUNKS - 1);
       const int row = f >> 3, col = k0 + (f & 7) * 8;
       const int q = min(q0 + row, q_last);
-      const uint4 v = *reinterpret_cast<const uint4*>(queries + (size_t)q * d + min(col, d - 8));
+      const uint4 v = *reinterpret_cast<const uint4*>(emb_at(queries, q, min(col, d - 8)));
       rb[c] = col < d ? v : make_uint4(0, 0, 0, 0);
     }
   }
@@ -115,9 +119,9 @@ __device__ __forceinline__ void mfma_slice(floatx16 (&acc)[2][NQT], const uint16
 // Scores of one step: acc[u][t][v] = S[h][q] with
 //   h = h0 + 64w + 32u + 8(v/4) + 4*half + (v%4),  q = q0 + 32t + l32.
 template <int NQT>
-__device__ __forceinline__ void gemm_step(floatx16 (&acc)[2][NQT], const uint16_t* __restrict__ hist,
-                                          int h0, int h_end, const uint16_t* __restrict__ queries,
-                                          int q0, int Q, int d, uint16_t* a_tile, uint16_t* b_tile) {
+__device__ __forceinline__ void gemm_step(floatx16 (&acc)[2][NQT], const EmbView& hist, int h0, int h_end,
+                                          const EmbView& queries, int q0, int Q, int d, uint16_t* a_tile,
+                                          uint16_t* b_tile) {
   const int lane = (int)lane_id();
   const int w = threadIdx.x / kWave;
   const int l32 = lane & 31, half = lane >> 5;
@@ -190,7 +194,7 @@ __device__ uint64_t merge_into_list(uint64_t* list, const uint64_t* buf, int n_b
 // ------------------------------------------------------------------------
 template <int NQT>
 __global__ void __launch_bounds__(kThreads, 1) threshold_sample_kernel(
-    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    EmbView queries, int Q, EmbView hist, int N, int d,
     int sample_every, int n_samples, float* __restrict__ gm) {
   constexpr int BQ = 32 * NQT;
   __shared__ __align__(16) uint16_t a_tile[kStepRows * kRowE];
@@ -242,7 +246,7 @@ struct TopkSmem {
 
 template <int NQT, int KL>
 __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
-    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    EmbView queries, int Q, EmbView hist, int N, int d,
     int k, int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0,
     const int* __restrict__ only_flagged, uint64_t* __restrict__ partial) {
   constexpr int BQ = 32 * NQT;
@@ -567,9 +571,9 @@ __device__ __forceinline__ void pin(floatx16& x) { asm volatile("" : "+a"(x)); }
 // Rows past N - 1 and queries past Q - 1 are read clamped (their scores are
 // meaningless and must be masked by the caller). Requires d % 32 == 0.
 template <class Epi>
-__device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, int h_first, int h_stride,
-                                      int n_steps, int h_limit, const uint16_t* __restrict__ queries, int Q,
-                                      int q0, int d, char* lds, Epi& epi) {
+__device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, int h_stride, int n_steps,
+                                      int h_limit, const EmbView& queries, int Q, int q0, int d, char* lds,
+                                      Epi& epi) {
   const int lane = (int)lane_id();
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int wh = w >> 1, wq = w & 1;
@@ -586,7 +590,9 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
   const bool hist_side = w < 2;
   const int r0 = 128 * (w & 1) + (lane >> 2);
   const uint32_t cb = (uint32_t)(((lane & 3) ^ swz(lane >> 2)) * 16);
-  const uint32_t row_bytes = (uint32_t)d * 2u;
+  // Bytes between rows of this wave's operand and between its 32-column slices.
+  const uint32_t row_bytes = (uint32_t)((hist_side ? hist.row : queries.row) * 2);
+  const long long slice_bytes = (hist_side ? hist.panel : queries.panel) * 2;
   int ld_step = 0, ld_kt = 0;
   const char* src = nullptr;                  // source of slice ld_kt of step ld_step
   uint32_t off[kLoads];                       // per-lane byte offsets within a slice
@@ -594,10 +600,10 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
     int last;
     if (hist_side) {
       const int base_row = h_first + ld_step * h_stride;
-      src = reinterpret_cast<const char*>(hist + (size_t)base_row * d);
+      src = reinterpret_cast<const char*>(emb_at(hist, base_row, 0));
       last = N - 1 - base_row;
     } else {
-      src = reinterpret_cast<const char*>(queries + (size_t)q0 * d);
+      src = reinterpret_cast<const char*>(emb_at(queries, q0, 0));
       last = Q - 1 - q0;
     }
 #pragma unroll
@@ -609,7 +615,7 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
     load_to_lds_if(src, off[i], __builtin_amdgcn_readfirstlane(m0), __builtin_amdgcn_readfirstlane(enabled));
   };
   auto advance = [&]() {
-    src += kKT * 2;
+    src += slice_bytes;
     if (++ld_kt == nk) {
       ld_kt = 0;
       ++ld_step;
@@ -720,7 +726,7 @@ __device__ __forceinline__ void sweep(const uint16_t* __restrict__ hist, int N, 
 // kernel): block (tile, y) runs samples y * spb .. of the sample list,
 // sample s being step s * sample_every; every sampled step is whole.
 __global__ void __launch_bounds__(kThreads, 1) threshold_sample_ring_kernel(
-    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    EmbView queries, int Q, EmbView hist, int N, int d,
     int sample_every, int n_samples, int spb, float* __restrict__ gm) {
   __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
   const int q0 = blockIdx.x * ring::kBQ;
@@ -754,7 +760,7 @@ __global__ void __launch_bounds__(kThreads, 1) threshold_sample_ring_kernel(
 // segment [q][chunk][0..seg_cap) (position from an LDS counter); the true
 // count goes to seg_count[q][chunk] even when the segment overflows.
 __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
-    const uint16_t* __restrict__ queries, int Q, const uint16_t* __restrict__ hist, int N, int d,
+    EmbView queries, int Q, EmbView hist, int N, int d,
     int chunk_rows, int n_chunks, int q_tiles, int q_groups, const float* __restrict__ theta0,
     int seg_cap, uint64_t* __restrict__ seg, int* __restrict__ seg_count) {
   __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
@@ -918,7 +924,7 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
 }
 
 template <int NQT, int KL>
-hipError_t launch_lists(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+hipError_t launch_lists(EmbView queries, int Q, EmbView hist, int N, int d, int k,
                         const SimTopkPlan& p, const float* theta0, const int* only_flagged,
                         uint64_t* partial, hipStream_t stream) {
   LaunchScope scope(only_flagged ? "sim_topk_fallback" : "sim_topk", stream);
@@ -928,7 +934,7 @@ hipError_t launch_lists(const uint16_t* queries, int Q, const uint16_t* hist, in
   return hipGetLastError();
 }
 
-hipError_t launch_theta(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int k,
                         const SimTopkPlan& p, int q_tiles, bool big, float* gm, float* theta0,
                         hipStream_t stream) {
   {
@@ -1026,7 +1032,7 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   return p;
 }
 
-hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d, int k,
                              const SimTopkPlan& p, void* workspace, int32_t* ids, float* sims,
                              hipStream_t stream) {
   if (Q == 0) return hipSuccess;

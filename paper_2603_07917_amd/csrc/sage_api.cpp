@@ -211,6 +211,42 @@ SAGE_API int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_st
   return hip_status(sage::launch_ingest_bf16(src, n, dst, (hipStream_t)stream), "ingest_bf16 launch");
 }
 
+namespace {
+int check_panels_args(const char* fn, const void* src, int rows, int d, const void* dst) {
+  if (rows < 0) return fail(SAGE_EINVAL, "%s: rows=%d is negative", fn, rows);
+  if (rows > (1 << 29)) return fail(SAGE_EINVAL, "%s: rows=%d above 2^29", fn, rows);
+  if (d < 32 || d % 32 != 0) return fail(SAGE_EINVAL, "%s: d=%d must be a positive multiple of 32", fn, d);
+  if (rows == 0) return SAGE_OK;
+  if (!src || !dst) return fail(SAGE_EINVAL, "%s: NULL pointer", fn);
+  if (!aligned16(src) || !aligned16(dst)) return fail(SAGE_EINVAL, "%s: misaligned pointer", fn);
+  return SAGE_OK;
+}
+}  // namespace
+
+SAGE_API int sage_ingest_bf16_panels(const float* src, int rows, int d, uint16_t* dst, sage_stream_t stream) {
+  int st = check_panels_args("sage_ingest_bf16_panels", src, rows, d, dst);
+  if (st != SAGE_OK || rows == 0) return st == SAGE_OK ? ok() : st;
+  const char* s0 = reinterpret_cast<const char*>(src);
+  const char* d0 = reinterpret_cast<const char*>(dst);
+  const size_t n = (size_t)rows * d;
+  if (s0 < d0 + n * sizeof(uint16_t) && d0 < s0 + n * sizeof(float))
+    return fail(SAGE_EINVAL, "sage_ingest_bf16_panels: src and dst overlap");
+  if ((st = check_device()) != SAGE_OK) return st;
+  return hip_status(sage::launch_ingest_panels(src, rows, d, dst, (hipStream_t)stream), "ingest_panels launch");
+}
+
+SAGE_API int sage_panels_from_rows(const uint16_t* src, int rows, int d, uint16_t* dst, sage_stream_t stream) {
+  int st = check_panels_args("sage_panels_from_rows", src, rows, d, dst);
+  if (st != SAGE_OK || rows == 0) return st == SAGE_OK ? ok() : st;
+  const char* s0 = reinterpret_cast<const char*>(src);
+  const char* d0 = reinterpret_cast<const char*>(dst);
+  const size_t bytes = (size_t)rows * d * sizeof(uint16_t);
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(SAGE_EINVAL, "sage_panels_from_rows: src and dst overlap");
+  if ((st = check_device()) != SAGE_OK) return st;
+  return hip_status(sage::launch_panels_from_rows(src, rows, d, dst, (hipStream_t)stream),
+                    "panels_from_rows launch");
+}
+
 SAGE_API int sage_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
                                int capacity, uint16_t* ring_emb, int32_t* ring_len, sage_stream_t stream) {
   if (n < 0) return fail(SAGE_EINVAL, "n=%d is negative", n);
@@ -250,11 +286,14 @@ SAGE_API size_t sage_predict_workspace_bytes(int Q, int N, int d, int k, int B) 
   return sage::plan_sim_topk(Q, N, d, k).workspace_bytes();
 }
 
-SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_emb,
-                          const int32_t* hist_len, int N, int d, int k, float tau,
-                          const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,
-                          int32_t* counts, float* mass, void* workspace, size_t workspace_bytes,
-                          sage_stream_t stream) {
+SAGE_API int sage_predict_layout(const uint16_t* queries, int query_layout, int Q, const uint16_t* hist_emb,
+                                 int hist_layout, const int32_t* hist_len, int N, int d, int k, float tau,
+                                 const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,
+                                 int32_t* counts, float* mass, void* workspace, size_t workspace_bytes,
+                                 sage_stream_t stream) {
+  for (int layout : {query_layout, hist_layout})
+    if (layout != SAGE_LAYOUT_ROWS && layout != SAGE_LAYOUT_PANELS)
+      return fail(SAGE_EINVAL, "layout=%d is not a SAGE_LAYOUT_* value", layout);
   int st = check_predict_sizes(Q, N, d, k, B);
   if (st != SAGE_OK) return st;
   if ((st = check_tau(tau)) != SAGE_OK) return st;
@@ -273,11 +312,23 @@ SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_e
   if (!aligned16(workspace)) return fail(SAGE_EINVAL, "sage_predict: workspace is not 16-byte aligned");
   if ((st = check_device()) != SAGE_OK) return st;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = sage::launch_neighbours(queries, Q, hist_emb, N, d, k, plan, workspace, nbr_ids,
-                                         nbr_sims, s);
+  const sage::EmbView qv = query_layout == SAGE_LAYOUT_PANELS ? sage::panels_view(queries, Q)
+                                                              : sage::rows_view(queries, d);
+  const sage::EmbView hv = hist_layout == SAGE_LAYOUT_PANELS ? sage::panels_view(hist_emb, N)
+                                                             : sage::rows_view(hist_emb, d);
+  hipError_t e = sage::launch_neighbours(qv, Q, hv, N, d, k, plan, workspace, nbr_ids, nbr_sims, s);
   if (e != hipSuccess) return hip_status(e, "neighbour search launch");
   e = sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, 0, counts, mass, s);
   return hip_status(e, "hist launch");
+}
+
+SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_emb,
+                          const int32_t* hist_len, int N, int d, int k, float tau,
+                          const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,
+                          int32_t* counts, float* mass, void* workspace, size_t workspace_bytes,
+                          sage_stream_t stream) {
+  return sage_predict_layout(queries, SAGE_LAYOUT_ROWS, Q, hist_emb, SAGE_LAYOUT_ROWS, hist_len, N, d, k, tau,
+                             bin_edges, B, nbr_ids, nbr_sims, counts, mass, workspace, workspace_bytes, stream);
 }
 
 static int histogram_impl(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,

@@ -19,6 +19,19 @@ struct LaunchScope {
   hipStream_t stream_;
 };
 
+// A matrix of bf16 embeddings (raw bits), `rows` x d: element (r, c) sits at
+// base[(c / 32) * panel + r * row + c % 32]. Row-major [rows, d]: panel = 32,
+// row = d. Panel-major [d / 32][rows][32]: panel = 32 * rows, row = 32; one
+// 32-column slice of consecutive rows is then contiguous, so a load of 16
+// rows of a slice covers whole 128-byte lines.
+struct EmbView {
+  const uint16_t* base;
+  long long panel;
+  long long row;
+};
+inline EmbView rows_view(const uint16_t* base, int d) { return EmbView{base, 32, (long long)d}; }
+inline EmbView panels_view(const uint16_t* base, int rows) { return EmbView{base, 32LL * rows, 32}; }
+
 // Launch plan of the neighbour search (threshold pre-pass, search, merge).
 struct SimTopkPlan {
   // exact per-chunk lists (the path for k > 64, and the fallback of the filtered path)
@@ -45,6 +58,9 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
 // Launchers: each enqueues kernels on `stream` and returns the HIP status of
 // the launch (hipSuccess or the first error).
 hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream);
+// [rows, d] -> panel-major bf16: from fp32 (rounded to nearest even) or from bf16 bits.
+hipError_t launch_ingest_panels(const float* src, int rows, int d, uint16_t* dst, hipStream_t stream);
+hipError_t launch_panels_from_rows(const uint16_t* src, int rows, int d, uint16_t* dst, hipStream_t stream);
 hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
                                int cap, uint16_t* ring_emb, int32_t* ring_len, hipStream_t stream);
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
@@ -65,7 +81,7 @@ hipError_t launch_index(const float* mass, const float* cost, const int32_t* pro
 size_t rank_workspace_bytes(int Q);
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream);
 // Neighbours of every query: ids [Q, k] and sims [Q, k] (sorted, padded).
-hipError_t launch_neighbours(const uint16_t* queries, int Q, const uint16_t* hist, int N, int d, int k,
+hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d, int k,
                              const SimTopkPlan& plan, void* workspace, int32_t* ids, float* sims,
                              hipStream_t stream);
 // Merge of per-chunk lists; with `only_flagged`, queries whose flag is 0 are skipped.

@@ -38,6 +38,9 @@ def load_library():
         "sage_ingest_bf16": (I, [P, Z, P, S]),
         "sage_predict_workspace_bytes": (Z, [I, I, I, I, I]),
         "sage_predict": (I, [P, I, P, P, I, I, I, F, P, I, P, P, P, P, P, Z, S]),
+        "sage_predict_layout": (I, [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, P, Z, S]),
+        "sage_ingest_bf16_panels": (I, [P, I, I, P, S]),
+        "sage_panels_from_rows": (I, [P, I, I, P, S]),
         "sage_histogram": (I, [P, P, I, I, P, I, F, P, I, P, P, S]),
         "sage_cost": (I, [P, I, P, I, P, S]),
         "sage_index": (I, [P, P, P, P, I, I, P, P, S]),
@@ -94,12 +97,44 @@ def _dev(t: torch.Tensor, dtype, name: str, ndim: Optional[int] = None) -> torch
 
 
 # ------------------------------------------------------------------ stages
-def ingest_bf16(x: torch.Tensor) -> torch.Tensor:
-    """fp32 embeddings -> bf16 store (round to nearest even), on the device."""
+# Layouts of an embedding matrix of R rows x d columns: "rows" is a 2-D tensor
+# [R, d]; "panels" is a 3-D tensor [d / 32, R, 32] (32-column panels, each
+# holding its columns of every row contiguously: the fast layout for search).
+LAYOUTS = {"rows": 0, "panels": 1}
+
+
+def ingest_bf16(x: torch.Tensor, layout: str = "rows") -> torch.Tensor:
+    """fp32 embeddings -> bf16 (round to nearest even), on the device; with
+    layout="panels", x must be [R, d] and the result is [d / 32, R, 32]."""
     _dev(x, torch.float32, "x")
-    out = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
-    _check(load_library().sage_ingest_bf16(_ptr(x), x.numel(), _ptr(out), _stream()))
+    if layout == "rows":
+        out = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+        _check(load_library().sage_ingest_bf16(_ptr(x), x.numel(), _ptr(out), _stream()))
+        return out
+    if layout != "panels" or x.dim() != 2 or x.shape[1] % 32 != 0:
+        raise SageError("panels ingest takes a 2-D [R, d] tensor with d % 32 == 0")
+    R, d = x.shape
+    out = torch.empty((d // 32, R, 32), dtype=torch.bfloat16, device=x.device)
+    _check(load_library().sage_ingest_bf16_panels(_ptr(x), R, d, _ptr(out), _stream()))
     return out
+
+
+def to_panels(x: torch.Tensor) -> torch.Tensor:
+    """bf16 [R, d] row-major -> [d / 32, R, 32] panel-major (bits unchanged)."""
+    _dev(x, torch.bfloat16, "x", 2)
+    R, d = x.shape
+    out = torch.empty((d // 32, R, 32), dtype=torch.bfloat16, device=x.device)
+    _check(load_library().sage_panels_from_rows(_ptr(x), R, d, _ptr(out), _stream()))
+    return out
+
+
+def emb_shape(x: torch.Tensor):
+    """(rows, d, layout code) of a bf16 embedding matrix in either layout."""
+    if x.dim() == 2:
+        return x.shape[0], x.shape[1], LAYOUTS["rows"]
+    if x.dim() == 3 and x.shape[2] == 32:
+        return x.shape[1], x.shape[0] * 32, LAYOUTS["panels"]
+    raise SageError("embeddings must be [R, d] (rows) or [d / 32, R, 32] (panels)")
 
 
 def predict_workspace_bytes(Q: int, N: int, d: int, k: int, B: int) -> int:
@@ -109,15 +144,16 @@ def predict_workspace_bytes(Q: int, N: int, d: int, k: int, B: int) -> int:
 def predict(queries: torch.Tensor, hist_emb: torch.Tensor, hist_len: torch.Tensor, k: int,
             tau: float, bin_edges: torch.Tensor, workspace: Optional[torch.Tensor] = None,
             out=None):
-    """Neighbours, per-bin counts and similarity-weighted masses for each query."""
-    _dev(queries, torch.bfloat16, "queries", 2)
-    _dev(hist_emb, torch.bfloat16, "hist_emb", 2)
+    """Neighbours, per-bin counts and similarity-weighted masses for each query.
+    queries and hist_emb may each be row-major [R, d] or panel-major [d / 32, R, 32]."""
+    _dev(queries, torch.bfloat16, "queries")
+    _dev(hist_emb, torch.bfloat16, "hist_emb")
     _dev(hist_len, torch.int32, "hist_len", 1)
     _dev(bin_edges, torch.float64, "bin_edges", 1)
-    Q, d = queries.shape
-    N = hist_emb.shape[0]
+    Q, d, q_layout = emb_shape(queries)
+    N, d_h, h_layout = emb_shape(hist_emb)
     B = bin_edges.shape[0] - 1
-    if hist_emb.shape[1] != d or hist_len.shape[0] != N:
+    if d_h != d or hist_len.shape[0] != N:
         raise SageError("shape mismatch between queries, hist_emb and hist_len")
     dev = queries.device
     need = predict_workspace_bytes(Q, N, d, k, B)
@@ -129,10 +165,10 @@ def predict(queries: torch.Tensor, hist_emb: torch.Tensor, hist_len: torch.Tenso
                torch.empty((Q, B), dtype=torch.int32, device=dev),
                torch.empty((Q, B), dtype=torch.float32, device=dev))
     ids, sims, counts, mass = out
-    _check(load_library().sage_predict(
-        _ptr(queries), Q, _ptr(hist_emb), _ptr(hist_len), N, d, k, float(tau), _ptr(bin_edges), B,
-        _ptr(ids), _ptr(sims), _ptr(counts), _ptr(mass), _ptr(workspace), workspace.numel(),
-        _stream()))
+    _check(load_library().sage_predict_layout(
+        _ptr(queries), q_layout, Q, _ptr(hist_emb), h_layout, _ptr(hist_len), N, d, k, float(tau),
+        _ptr(bin_edges), B, _ptr(ids), _ptr(sims), _ptr(counts), _ptr(mass), _ptr(workspace),
+        workspace.numel(), _stream()))
     return ids, sims, counts, mass
 
 
@@ -314,13 +350,18 @@ class Store:
 
     Holds the bf16 embeddings, the recorded output lengths and the bin edges
     on the device, and reuses the predict / rank workspaces across calls so
-    that a steady-state decision allocates nothing new.
+    that a steady-state decision allocates nothing new. fp32 embeddings
+    (store and queries) are ingested in `layout` ("panels" by default: the
+    fast one for the search; results are identical).
     """
 
     def __init__(self, hist_emb: torch.Tensor, hist_len: torch.Tensor, bin_edges: torch.Tensor,
-                 bin_repr: torch.Tensor, k: int, tau: float = 0.8):
+                 bin_repr: torch.Tensor, k: int, tau: float = 0.8, layout: str = "panels"):
+        if layout not in LAYOUTS:
+            raise SageError(f"unknown layout {layout!r}")
+        self.layout = layout
         if hist_emb.dtype == torch.float32:
-            hist_emb = ingest_bf16(hist_emb.contiguous())
+            hist_emb = ingest_bf16(hist_emb.contiguous(), layout)
         self.hist_emb = hist_emb
         self.hist_len = hist_len
         self.bin_edges = bin_edges
@@ -331,7 +372,7 @@ class Store:
         self._rank_ws = torch.empty(16, dtype=torch.uint8, device=hist_emb.device)
 
     def _workspace(self, Q: int) -> torch.Tensor:
-        N, d = self.hist_emb.shape
+        N, d, _ = emb_shape(self.hist_emb)
         need = predict_workspace_bytes(Q, N, d, self.k, self.bin_edges.shape[0] - 1)
         if self._ws.numel() < need:
             self._ws = torch.empty(need, dtype=torch.uint8, device=self.hist_emb.device)
@@ -339,9 +380,10 @@ class Store:
 
     def predict(self, queries: torch.Tensor, out=None):
         if queries.dtype == torch.float32:
-            queries = ingest_bf16(queries.contiguous())
+            queries = ingest_bf16(queries.contiguous(), self.layout)
+        Q = emb_shape(queries)[0]
         return predict(queries, self.hist_emb, self.hist_len, self.k, self.tau, self.bin_edges,
-                       workspace=self._workspace(queries.shape[0]), out=out)
+                       workspace=self._workspace(Q), out=out)
 
     def decide(self, queries: torch.Tensor, prompt_len: torch.Tensor, out=None):
         """One scheduling decision for a batch: predict, cost+index, rank."""
@@ -382,7 +424,7 @@ class RingStore(Store):
         self.ring_emb = torch.zeros((capacity, d), dtype=torch.bfloat16, device=dev)
         self.ring_len = torch.zeros(capacity, dtype=torch.int32, device=dev)
         self.total = 0
-        super().__init__(self.ring_emb[:1], self.ring_len[:1], bin_edges, bin_repr, k, tau)
+        super().__init__(self.ring_emb[:1], self.ring_len[:1], bin_edges, bin_repr, k, tau, layout="rows")
 
     @property
     def rows(self) -> int:

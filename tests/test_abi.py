@@ -42,6 +42,9 @@ def lib():
     lib.sage_cost.argtypes = [P, I, P, I, P, P]
     lib.sage_histogram.argtypes = [P, P, I, I, P, I, F, P, I, P, P, P]
     lib.sage_ingest_bf16.argtypes = [P, Z, P, P]
+    lib.sage_ingest_bf16_panels.argtypes = [P, I, I, P, P]
+    lib.sage_panels_from_rows.argtypes = [P, I, I, P, P]
+    lib.sage_predict_layout.argtypes = [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, P, Z, P]
     lib.sage_status_string.restype = ctypes.c_char_p
     lib.sage_last_error.restype = ctypes.c_char_p
     return lib
@@ -90,6 +93,33 @@ def test_predict_rejects_bad_sizes(lib, kw):
 def test_predict_rejects_null_and_misaligned(lib, name):
     assert _predict(lib, ptrs={name: None}) == SAGE_EINVAL
     assert _predict(lib, ptrs={name: A + 4}) == SAGE_EINVAL
+
+
+def test_predict_layout_validation(lib):
+    def call(ql=0, hl=0, **kw):
+        a = dict(Q=4, N=100, d=64, k=8, tau=0.8, B=16)
+        a.update(kw)
+        return lib.sage_predict_layout(A, ql, a["Q"], A, hl, A, a["N"], a["d"], a["k"], a["tau"], A, a["B"],
+                                       A, A, A, A, A, 1 << 30, None)
+    for ql, hl in [(2, 0), (0, 2), (-1, 1), (1, -1)]:
+        assert call(ql, hl) == SAGE_EINVAL
+        assert b"layout" in lib.sage_last_error()
+    assert call(1, 1, d=48) == SAGE_EINVAL
+    assert call(1, 1, k=0) == SAGE_EINVAL
+    assert call(1, 1, Q=0) == SAGE_OK
+
+
+def test_panels_ingest_validation(lib):
+    for fn in (lib.sage_ingest_bf16_panels, lib.sage_panels_from_rows):
+        assert fn(A, -1, 64, A + 0x100000, None) == SAGE_EINVAL
+        assert fn(A, 10, 48, A + 0x100000, None) == SAGE_EINVAL
+        assert fn(A, 10, 0, A + 0x100000, None) == SAGE_EINVAL
+        assert fn(None, 10, 64, A + 0x100000, None) == SAGE_EINVAL
+        assert fn(A + 4, 10, 64, A + 0x100000, None) == SAGE_EINVAL
+        assert fn(A, 10, 64, A + 8, None) == SAGE_EINVAL          # misaligned
+        assert fn(A, 10, 64, A + 16, None) == SAGE_EINVAL         # overlapping
+        assert fn(A, 1 << 30, 64, A + 0x100000, None) == SAGE_EINVAL
+        assert fn(None, 0, 64, None, None) == SAGE_OK              # nothing to do
 
 
 def test_predict_workspace_too_small(lib):

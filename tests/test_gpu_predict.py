@@ -71,6 +71,39 @@ def test_predict_small_vs_oracle(Q, N, d, k, B):
     parity.check_predict(ids, sims, counts, mass, S, w.hist_len, w.bin_edges, 0.8, k)
 
 
+def test_panels_ingest_bit_exact():
+    """The panel-major store holds exactly the row-major bf16 bits, rearranged."""
+    rng = np.random.default_rng(7)
+    for R, d in [(1, 32), (1000, 96), (4099, 768)]:
+        x = dev(rng.standard_normal((R, d)).astype(np.float32))
+        rows = sage.ingest_bf16(x)
+        pan = sage.ingest_bf16(x, "panels")
+        expect = rows.view(R, d // 32, 32).permute(1, 0, 2).contiguous()
+        assert tuple(pan.shape) == (d // 32, R, 32)
+        assert torch.equal(pan.view(torch.int16), expect.view(torch.int16))
+        assert torch.equal(sage.to_panels(rows).view(torch.int16), expect.view(torch.int16))
+
+
+LAYOUT_CASES = CASES + [(12, 12000, 64, 8, 16)]
+
+
+@pytest.mark.parametrize("Q,N,d,k,B", LAYOUT_CASES)
+def test_predict_panels_identical_to_rows(Q, N, d, k, B):
+    """Every search path (filtered, exact lists, two-level merge, fallback)
+    gives bit-identical outputs on panel-major and row-major operands."""
+    print(f"case Q={Q} N={N} d={d} k={k} B={B}", flush=True)
+    w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=B, seed=Q + N + d + k, clusters=6)
+    if (Q, N) == (12, 12000):                      # overflowing candidates: the exact fallback
+        w.hist_emb[:6000] = w.hist_emb[6000]
+        w.queries[:6] = w.hist_emb[6000]
+    qf, hf, hl, be = dev(w.queries), dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges)
+    ref = [host(t) for t in sage.predict(sage.ingest_bf16(qf), sage.ingest_bf16(hf), hl, k, 0.8, be)]
+    for ql, hlay in [("panels", "panels"), ("rows", "panels"), ("panels", "rows")]:
+        out = sage.predict(sage.ingest_bf16(qf, ql), sage.ingest_bf16(hf, hlay), hl, k, 0.8, be)
+        for a, b in zip(ref, [host(t) for t in out]):
+            assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), (ql, hlay)
+
+
 def test_predict_duplicate_rows_lower_id_first():
     # identical history rows score identically in fp32: the lower index must come first
     w = workloads.small_predict(Q=8, N=600, d=64, k=16, B=16, seed=5, clusters=2)
