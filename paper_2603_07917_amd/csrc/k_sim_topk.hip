@@ -510,7 +510,7 @@ __global__ void __launch_bounds__(256) threshold_radix_kernel(const float* __res
 namespace ring {
 
 constexpr int kKT = 32;                          // bf16 columns per slice
-constexpr int kStages = 4;
+constexpr int kStages = 4;                       // a power of two (stage = g & (kStages - 1))
 constexpr int kStageBytes = 512 * kKT * 2;       // 32 KiB
 constexpr int kBQ = 256;                         // queries per tile
 constexpr int kLoads = 8;                        // 16-byte loads per lane per slice
@@ -611,8 +611,12 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
   };
   // Load i (0..7) of slice g into its stage; then advance to the next slice.
   auto issue_one = [&](int g, int i, int enabled) {
-    const uint32_t m0 = lds0 + (uint32_t)((g % kStages) * kStageBytes + (w * kLoads + i) * 1024);
+    const uint32_t m0 = lds0 + (uint32_t)((g & (kStages - 1)) * kStageBytes + (w * kLoads + i) * 1024);
     load_to_lds_if(src, off[i], __builtin_amdgcn_readfirstlane(m0), __builtin_amdgcn_readfirstlane(enabled));
+  };
+  auto issue_always = [&](int g, int i) {
+    const uint32_t m0 = lds0 + (uint32_t)((g & (kStages - 1)) * kStageBytes + (w * kLoads + i) * 1024);
+    load_to_lds(src, off[i], __builtin_amdgcn_readfirstlane(m0));
   };
   auto advance = [&]() {
     src += slice_bytes;
@@ -639,7 +643,7 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
     b_off[kk] = (uint32_t)((256 + 128 * wq + l32) * 64) + pos;
   }
   auto read = [&](int g, int kk, Frags& f) {
-    const char* stage = lds + (g % kStages) * kStageBytes;
+    const char* stage = lds + (g & (kStages - 1)) * kStageBytes;
 #pragma unroll
     for (int u = 0; u < 4; ++u) f.a[u] = *reinterpret_cast<const bf16x8*>(stage + a_off[kk] + u * 2048);
 #pragma unroll
@@ -647,7 +651,7 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
   };
   // Piece p of the fragments: A tile p (p < 4) or B tile p - 4.
   auto read_piece = [&](int g, int kk, int p, Frags& f) {
-    const char* stage = lds + (g % kStages) * kStageBytes;
+    const char* stage = lds + (g & (kStages - 1)) * kStageBytes;
     if (p < 4) f.a[p] = *reinterpret_cast<const bf16x8*>(stage + a_off[kk] + p * 2048);
     else f.b[p - 4] = *reinterpret_cast<const bf16x8*>(stage + b_off[kk] + (p - 4) * 2048);
   };
@@ -675,15 +679,18 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
     //  * The eight loads of slice g + kAhead (whose stage was last read in
     //    slice g - 1) go out four in each half, which keeps the address unit
     //    evenly busy.
-    auto slice = [&](bool first) {
-      const int more = g + kAhead < total;
+    auto slice = [&](bool first, bool steady) {
+      const int more = steady ? 1 : (g + kAhead < total);
       const floatx16 zero = {};
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int u = j >> 2, t = j & 3;
         acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0.a[u], f0.b[t], first ? zero : acc[u][t], 0, 0, 0);
         if (j < 8) read_piece(g, 1, j, f1);
-        if (t == 3) issue_one(g + kAhead, u, more);
+        if (t == 3) {
+          if (steady) issue_always(g + kAhead, u);
+          else issue_one(g + kAhead, u, more);
+        }
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -691,18 +698,25 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-      const int after = (g + 2 < total ? kLoads : 0) + (more ? kLoads / 2 : 0);
-      if (after == 0) wait_loads<0>();
-      else if (after == kLoads / 2) wait_loads<kLoads / 2>();
-      else if (after == kLoads) wait_loads<kLoads>();
-      else wait_loads<kLoads + kLoads / 2>();
+      if (steady) {
+        wait_loads<kLoads + kLoads / 2>();
+      } else {
+        const int after = (g + 2 < total ? kLoads : 0) + (more ? kLoads / 2 : 0);
+        if (after == 0) wait_loads<0>();
+        else if (after == kLoads / 2) wait_loads<kLoads / 2>();
+        else if (after == kLoads) wait_loads<kLoads>();
+        else wait_loads<kLoads + kLoads / 2>();
+      }
       barrier();
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int u = j >> 2, t = j & 3;
         acc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1.a[u], f1.b[t], acc[u][t], 0, 0, 0);
         if (j < 8) read_piece(g + 1, 0, j, f0);
-        if (t == 3) issue_one(g + kAhead, kLoads / 2 + u, more);
+        if (t == 3) {
+          if (steady) issue_always(g + kAhead, kLoads / 2 + u);
+          else issue_one(g + kAhead, kLoads / 2 + u, more);
+        }
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -713,8 +727,15 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
       if (more) advance();
       ++g;
     };
-    slice(true);
-    for (int kt = 1; kt < nk; ++kt) slice(false);
+    // Every slice of a step before the last has its look-ahead slice inside
+    // the sweep (when a step has at least kAhead slices): no conditions.
+    if (nk >= kAhead && step + 1 < n_steps) {
+      slice(true, true);
+      for (int kt = 1; kt < nk; ++kt) slice(false, true);
+    } else {
+      slice(true, false);
+      for (int kt = 1; kt < nk; ++kt) slice(false, false);
+    }
     const int h0 = h_first + step * h_stride;
     epi(acc, h0, min(h_limit, h0 + 256));
   }
