@@ -437,64 +437,48 @@ __device__ __forceinline__ uint64_t fold_lists(uint64_t list, const uint64_t (&l
   return list;
 }
 
-// theta0: the k-th largest of a query's m (<= kMaxSamples * 16) group maxima,
-// found by a radix select on their monotone bits, one 8-bit digit per pass
-// from the top: count the values that match the digits fixed so far per next
-// digit (LDS atomics), then fix the digit whose suffix count reaches the rank
-// still wanted. Exact: the result is the k-th largest value itself.
-constexpr int kMaxGroupMaxima = 512 * 16;
-
-__global__ void __launch_bounds__(256) threshold_radix_kernel(const float* __restrict__ gm, int m, int k,
-                                                              float* __restrict__ theta0) {
-  __shared__ uint32_t vals[kMaxGroupMaxima];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t pick[2];                        // digit, count of values above it
-  const int q = blockIdx.x;
-  const int t = threadIdx.x;
+// theta0: the k-th largest of a query's m (<= 512 * 16) group maxima.
+// One wavefront per query; the query's m group maxima sit in registers as
+// monotone key bits, VPL per lane (lane l holds maxima l, l + 64, ...; past m:
+// key 0, below every real score). theta0 is the largest key T with at least
+// k keys >= T, built bit by bit from the top: each bit costs one compare per
+// key and a wave sum. That T is exactly the k-th largest key.
+template <int VPL>
+__global__ void __launch_bounds__(256) threshold_select_kernel(const float* __restrict__ gm, int Q, int m,
+                                                               int k, float* __restrict__ theta0) {
+  const int lane = (int)lane_id();
+  const int q = (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave);
+  if (q >= Q) return;
   const float* src = gm + (size_t)q * m;
-  for (int i = t; i < m; i += 256) vals[i] = f32_order_bits(src[i]);
-  if (t < 2) pick[t] = 0;
-  uint32_t prefix = 0, mask = 0;
-  int want = k;                                       // rank wanted among the matching values
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    hist[t] = 0;
-    __syncthreads();
-    for (int i = t; i < m; i += 256) {
-      const uint32_t v = vals[i];
-      if ((v & mask) == prefix) atomicAdd(&hist[(v >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    if (t < kWave) {                                  // suffix counts over the 256 digits
-      uint32_t c[4], run = 0;
+  uint32_t key[VPL];
 #pragma unroll
-      for (int j = 3; j >= 0; --j) { run += hist[4 * t + j]; c[j] = run; }   // within lane, high first
-      uint32_t above = 0;                             // sum of hist over lanes > t
-      {
-        uint32_t x = run;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-          const uint32_t y = __shfl_down(x, o, kWave);
-          if (t + o < kWave) x += y;
-        }
-        above = x - run;
-      }
-      // digit 4t + j has (above + c[j]) values >= it and (above + c[j] - hist) above it
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t ge = above + c[j];
-        const uint32_t gt = ge - hist[4 * t + j];
-        if (gt < (uint32_t)want && ge >= (uint32_t)want) { pick[0] = 4 * t + j; pick[1] = gt; }
-      }
-    }
-    __syncthreads();
-    prefix |= pick[0] << shift;
-    mask |= 255u << shift;
-    want -= (int)pick[1];
-    __syncthreads();
+  for (int i = 0; i < VPL; ++i) {
+    const int e = i * kWave + lane;
+    key[i] = e < m ? f32_order_bits(src[e]) : 0u;
   }
-  if (t == 0) theta0[q] = k <= m ? f32_from_order_bits(prefix) : -__builtin_inff();
+  // Every key lies in [lo, hi], and so does the answer: the bits above the
+  // highest one where lo and hi differ are fixed from the start.
+  uint32_t kmax = 0, kmin = 0xffffffffu;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    kmax = max(kmax, key[i]);
+    if (i * kWave + lane < m) kmin = min(kmin, key[i]);
+  }
+  const uint32_t hi = wave_max_dpp_u32(kmax), lo = wave_min_dpp_u32(kmin);
+  const int top = hi == lo ? -1 : 31 - __clz(hi ^ lo);
+  uint32_t T = top < 0 ? hi : hi & ~((2u << top) - 1u);
+  for (int bit = top; bit >= 0; --bit) {
+    const uint32_t c = T | (1u << bit);
+    uint32_t n0 = 0, n1 = 0;
+#pragma unroll
+    for (int i = 0; i < VPL; i += 2) {
+      n0 += key[i] >= c ? 1u : 0u;
+      n1 += key[i + 1] >= c ? 1u : 0u;
+    }
+    if (wave_sum_dpp_u32(n0 + n1) >= (uint32_t)k) T = c;
+  }
+  if (lane == 0) theta0[q] = k <= m ? f32_from_order_bits(T) : -__builtin_inff();
 }
-
 // ========================================================================
 // Filtered path for k <= 64.
 //
@@ -976,7 +960,15 @@ hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int 
   }
   const int m = p.n_samples * 16;
   LaunchScope scope("threshold_select", stream);
-  hipLaunchKernelGGL(threshold_radix_kernel, dim3(Q), dim3(256), 0, stream, gm, m, k, theta0);
+  const dim3 grid((Q + 3) / 4);                        // four queries (wavefronts) per workgroup
+  if (m <= 16 * kWave)
+    hipLaunchKernelGGL(threshold_select_kernel<16>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+  else if (m <= 32 * kWave)
+    hipLaunchKernelGGL(threshold_select_kernel<32>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+  else if (m <= 64 * kWave)
+    hipLaunchKernelGGL(threshold_select_kernel<64>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+  else
+    hipLaunchKernelGGL(threshold_select_kernel<128>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
   return hipGetLastError();
 }
 

@@ -155,6 +155,38 @@ __device__ __forceinline__ double last_lane_f64(double x) {
 // The inclusive value of the lane below (0 for lane 0): an exclusive prefix.
 __device__ __forceinline__ double wave_shift_up_dpp_f64(double x) { return dpp_f64<kDppWaveShr1>(0.0, x); }
 
+// Sum over the 64 lanes, returned as a wave-uniform value (DPP row scans,
+// then lane 63).
+__device__ __forceinline__ uint32_t wave_sum_dpp_u32(uint32_t x) {
+  x += dpp_u32<kDppRowShr1>(0u, x);
+  x += dpp_u32<kDppRowShr2>(0u, x);
+  x += dpp_u32<kDppRowShr4>(0u, x);
+  x += dpp_u32<kDppRowShr8>(0u, x);
+  x += dpp_u32<kDppRowBcast15, 0xa>(0u, x);
+  x += dpp_u32<kDppRowBcast31, 0xc>(0u, x);
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+}
+
+// Maximum and minimum over the 64 lanes, wave-uniform.
+__device__ __forceinline__ uint32_t wave_max_dpp_u32(uint32_t x) {
+  x = max(x, dpp_u32<kDppRowShr1>(x, x));
+  x = max(x, dpp_u32<kDppRowShr2>(x, x));
+  x = max(x, dpp_u32<kDppRowShr4>(x, x));
+  x = max(x, dpp_u32<kDppRowShr8>(x, x));
+  x = max(x, dpp_u32<kDppRowBcast15, 0xa>(x, x));
+  x = max(x, dpp_u32<kDppRowBcast31, 0xc>(x, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+}
+__device__ __forceinline__ uint32_t wave_min_dpp_u32(uint32_t x) {
+  x = min(x, dpp_u32<kDppRowShr1>(x, x));
+  x = min(x, dpp_u32<kDppRowShr2>(x, x));
+  x = min(x, dpp_u32<kDppRowShr4>(x, x));
+  x = min(x, dpp_u32<kDppRowShr8>(x, x));
+  x = min(x, dpp_u32<kDppRowBcast15, 0xa>(x, x));
+  x = min(x, dpp_u32<kDppRowBcast31, 0xc>(x, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+}
+
 __device__ __forceinline__ int wave_sum_i32(int x) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
