@@ -437,34 +437,45 @@ __device__ __forceinline__ uint64_t fold_lists(uint64_t list, const uint64_t (&l
   return list;
 }
 
-// theta0: the k-th largest of a query's m (<= 512 * 16) group maxima.
-// One wavefront per query; the query's m group maxima sit in registers as
-// monotone key bits, VPL per lane (lane l holds maxima l, l + 64, ...; past m:
-// key 0, below every real score). theta0 is the largest key T with at least
-// k keys >= T, built bit by bit from the top: each bit costs one compare per
-// key and a wave sum. That T is exactly the k-th largest key.
-template <int VPL>
-__global__ void __launch_bounds__(256) threshold_select_kernel(const float* __restrict__ gm, int Q, int m,
-                                                               int k, float* __restrict__ theta0) {
+// theta0: the k-th largest of a query's m (<= 512 * 16) group maxima, held
+// in registers as monotone key bits (VPL per lane; past m: key 0, below every
+// real score). theta0 is the largest key T with at least k keys >= T, built
+// bit by bit from the top: each bit costs one compare per key and a sum. That
+// T is exactly the k-th largest key. Every key lies in [lo, hi], and so does
+// the answer: the bits above the highest one where lo and hi differ are fixed
+// from the start.
+//
+// WAVES = 1: one wavefront per query, four queries per workgroup (many
+// queries). WAVES > 1: one workgroup of WAVES wavefronts per query, the sums
+// completed through LDS (few queries, where one wave per query would leave
+// the chip idle and each wave latency-bound).
+template <int VPL, int WAVES>
+__global__ void __launch_bounds__(256 * (WAVES > 1 ? WAVES / 4 : 1)) threshold_select_kernel(
+    const float* __restrict__ gm, int Q, int m, int k, float* __restrict__ theta0) {
+  __shared__ uint32_t part[2][WAVES > 1 ? WAVES : 1];
+  __shared__ uint32_t ext[2][WAVES > 1 ? WAVES : 1];
   const int lane = (int)lane_id();
-  const int q = (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave);
-  if (q >= Q) return;
+  const int w = (int)(threadIdx.x / kWave);
+  const int q = WAVES > 1 ? (int)blockIdx.x : (int)(blockIdx.x * (blockDim.x / kWave) + w);
+  if (q >= Q) return;                                   // whole wavefronts (WAVES = 1 only)
   const float* src = gm + (size_t)q * m;
+  const int first = WAVES > 1 ? w * VPL * kWave : 0;    // this wave's keys: first + i * 64 + lane
   uint32_t key[VPL];
-#pragma unroll
-  for (int i = 0; i < VPL; ++i) {
-    const int e = i * kWave + lane;
-    key[i] = e < m ? f32_order_bits(src[e]) : 0u;
-  }
-  // Every key lies in [lo, hi], and so does the answer: the bits above the
-  // highest one where lo and hi differ are fixed from the start.
   uint32_t kmax = 0, kmin = 0xffffffffu;
 #pragma unroll
   for (int i = 0; i < VPL; ++i) {
+    const int e = first + i * kWave + lane;
+    key[i] = e < m ? f32_order_bits(src[e]) : 0u;
     kmax = max(kmax, key[i]);
-    if (i * kWave + lane < m) kmin = min(kmin, key[i]);
+    if (e < m) kmin = min(kmin, key[i]);
   }
-  const uint32_t hi = wave_max_dpp_u32(kmax), lo = wave_min_dpp_u32(kmin);
+  uint32_t hi = wave_max_dpp_u32(kmax), lo = wave_min_dpp_u32(kmin);
+  if (WAVES > 1) {
+    if (lane == 0) { ext[0][w] = hi; ext[1][w] = lo; }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < WAVES; ++i) { hi = max(hi, ext[0][i]); lo = min(lo, ext[1][i]); }
+  }
   const int top = hi == lo ? -1 : 31 - __clz(hi ^ lo);
   uint32_t T = top < 0 ? hi : hi & ~((2u << top) - 1u);
   for (int bit = top; bit >= 0; --bit) {
@@ -473,11 +484,19 @@ __global__ void __launch_bounds__(256) threshold_select_kernel(const float* __re
 #pragma unroll
     for (int i = 0; i < VPL; i += 2) {
       n0 += key[i] >= c ? 1u : 0u;
-      n1 += key[i + 1] >= c ? 1u : 0u;
+      if (i + 1 < VPL) n1 += key[i + 1] >= c ? 1u : 0u;
     }
-    if (wave_sum_dpp_u32(n0 + n1) >= (uint32_t)k) T = c;
+    uint32_t n = wave_sum_dpp_u32(n0 + n1);
+    if (WAVES > 1) {                                    // partials alternate buffers: one barrier per bit
+      if (lane == 0) part[bit & 1][w] = n;
+      __syncthreads();
+      n = 0;
+#pragma unroll
+      for (int i = 0; i < WAVES; ++i) n += part[bit & 1][i];
+    }
+    if (n >= (uint32_t)k) T = c;
   }
-  if (lane == 0) theta0[q] = k <= m ? f32_from_order_bits(T) : -__builtin_inff();
+  if (lane == 0 && (WAVES == 1 || w == 0)) theta0[q] = k <= m ? f32_from_order_bits(T) : -__builtin_inff();
 }
 // ========================================================================
 // Filtered path for k <= 64.
@@ -960,15 +979,22 @@ hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int 
   }
   const int m = p.n_samples * 16;
   LaunchScope scope("threshold_select", stream);
-  const dim3 grid((Q + 3) / 4);                        // four queries (wavefronts) per workgroup
-  if (m <= 16 * kWave)
-    hipLaunchKernelGGL(threshold_select_kernel<16>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
-  else if (m <= 32 * kWave)
-    hipLaunchKernelGGL(threshold_select_kernel<32>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
-  else if (m <= 64 * kWave)
-    hipLaunchKernelGGL(threshold_select_kernel<64>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
-  else
-    hipLaunchKernelGGL(threshold_select_kernel<128>, grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+  if (Q < 512) {                                       // one 16-wave workgroup per query
+    if (m <= 2 * 16 * kWave)
+      hipLaunchKernelGGL((threshold_select_kernel<2, 16>), dim3(Q), dim3(1024), 0, stream, gm, Q, m, k, theta0);
+    else
+      hipLaunchKernelGGL((threshold_select_kernel<8, 16>), dim3(Q), dim3(1024), 0, stream, gm, Q, m, k, theta0);
+  } else {                                             // four queries (wavefronts) per workgroup
+    const dim3 grid((Q + 3) / 4);
+    if (m <= 16 * kWave)
+      hipLaunchKernelGGL((threshold_select_kernel<16, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+    else if (m <= 32 * kWave)
+      hipLaunchKernelGGL((threshold_select_kernel<32, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+    else if (m <= 64 * kWave)
+      hipLaunchKernelGGL((threshold_select_kernel<64, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+    else
+      hipLaunchKernelGGL((threshold_select_kernel<128, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+  }
   return hipGetLastError();
 }
 

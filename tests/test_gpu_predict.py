@@ -104,6 +104,25 @@ def test_predict_panels_identical_to_rows(Q, N, d, k, B):
             assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), (ql, hlay)
 
 
+@pytest.mark.parametrize("Q,N,d,k", [(600, 40000, 64, 32), (40, 40000, 64, 32), (600, 40000, 64, 100)])
+def test_predict_ignores_workspace_contents(Q, N, d, k):
+    """Outputs do not depend on what the workspace held before the call (every
+    intermediate, thresholds included, is written before it is read)."""
+    w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=32, seed=Q + k, clusters=6)
+    qb, hb = sage.ingest_bf16(dev(w.queries), "panels"), sage.ingest_bf16(dev(w.hist_emb), "panels")
+    hl, be = dev(w.hist_len), dev(w.bin_edges)
+    need = sage.predict_workspace_bytes(Q, N, d, k, 32)
+    outs = []
+    for fill in (0x00, 0x7F, 0xFF):
+        ws = torch.full((need,), fill, dtype=torch.uint8, device="cuda")
+        outs.append([host(t) for t in sage.predict(qb, hb, hl, k, 0.8, be, workspace=ws)])
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+    S = oracle_scores(w)
+    parity.check_predict(*outs[0], S, w.hist_len, w.bin_edges, 0.8, k)
+
+
 def test_predict_duplicate_rows_lower_id_first():
     # identical history rows score identically in fp32: the lower index must come first
     w = workloads.small_predict(Q=8, N=600, d=64, k=16, B=16, seed=5, clusters=2)
