@@ -837,12 +837,25 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
     for (int t = 0; t < 4; ++t) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) ring::pin(acc[u][t]);
-      uint32_t lo = 0, hi = 0;
+      // Bit v of mk[u] = [acc[u][t][v] > thr]: the sign of thr - s, shifted
+      // in with one funnel shift (no compare, so no serialisation on VCC).
+      // For finite scores the sign of the rounded difference is exact: -0
+      // only arises from a negative difference.
+      uint32_t mk[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int i = 31; i >= 0; --i) {
-        lo = 2 * lo + (acc[i >> 4][t][i & 15] > thr[t] ? 1u : 0u);
-        hi = 2 * hi + (acc[2 + (i >> 4)][t][i & 15] > thr[t] ? 1u : 0u);
+      for (int u = 0; u < 4; ++u) {
+        // The tile is copied out whole before use, so the 16 register reads
+        // and differences are independent rather than one chain through a
+        // single temporary.
+        floatx16 tv = acc[u][t];
+        asm volatile("" : "+v"(tv));
+        uint32_t sg[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sg[v] = __float_as_uint(thr[t] - tv[v]);
+#pragma unroll
+        for (int v = 15; v >= 0; --v) mk[u] = __builtin_amdgcn_alignbit(mk[u], sg[v], 31);
       }
+      const uint32_t lo = mk[0] | (mk[1] << 16), hi = mk[2] | (mk[3] << 16);
       uint64_t m = ((uint64_t)hi << 32) | lo;
       if (step_end - h0 < kStepRows) {                          // last, partial step
         uint64_t valid = 0;
