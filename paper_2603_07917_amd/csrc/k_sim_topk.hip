@@ -892,12 +892,12 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
   if (q0 + tid < Q) seg_count[(size_t)(q0 + tid) * n_chunks + chunk] = cnt[tid];
 }
 
-// Select kernel: one workgroup (4 waves) per query. Candidate p of the
-// query's concatenated segments is found by a search of the segment offsets
-// and read straight from global memory, 64 at a time per wave. Each wave keeps
-// its best 64 keys as a descending list across lanes: a group that beats the
-// list's last key is sorted (wave bitonic sort) and folded in with
-// C_i = max(A_i, B_{63-i}) and six half-cleaner stages. Wave 0 then folds in
+// Select kernel: one workgroup (4 waves) per query. Wave w reads the query's
+// segments w, w + 4, ... straight from global memory, 64 keys at a time. Each
+// wave keeps its best 64 keys as a descending list across lanes; keys that
+// beat the list's last key are gathered in LDS, and each 64 of them are
+// sorted (wave bitonic sort) and folded in with C_i = max(A_i, B_{63-i}) and
+// six half-cleaner stages. Wave 0 then folds in
 // the other three lists and writes the first k. A query with an overflowed
 // segment is flagged for the exact fallback and left untouched here.
 __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict__ seg,
@@ -907,6 +907,7 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
   __shared__ int off[kWave + 1];
   __shared__ int over;
   __shared__ uint64_t lists[4][kWave];
+  __shared__ uint64_t pend[4][2 * kWave];
   const int q = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = (int)lane_id();
@@ -931,25 +932,39 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
     return;
   }
   if (tid == 0) flags[q] = 0;
-  const int total = off[kWave];
   const uint64_t* src = seg + (size_t)q * n_chunks * seg_cap;
-  auto candidate = [&](int p) -> uint64_t {
-    if (p >= total) return kPadKey;
-    int lo = 0, hi = n_chunks - 1;                    // last segment with off <= p
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (off[mid] <= p) lo = mid;
-      else hi = mid - 1;
-    }
-    return src[(size_t)lo * seg_cap + (p - off[lo])];
-  };
+  // Keys that beat the list's current last key are packed into a per-wave
+  // LDS buffer (ballot positions); a sort-and-merge runs once 64 have
+  // gathered, instead of once per group that holds any of them. Wave w
+  // reads segments w, w + 4, ..., 64 consecutive keys at a time.
+  uint64_t* buf = pend[w];
   uint64_t list = kPadKey;
-  uint64_t next = candidate(w * kWave + lane);
-  for (int base = w * kWave; base < total; base += 4 * kWave) {
-    const uint64_t cur = next;
-    next = candidate(base + 4 * kWave + lane);        // prefetch
-    list = fold_group(list, cur);
+  int n_buf = 0;                                      // keys waiting in buf (wave-uniform, < 64)
+  for (int c = w; c < n_chunks; c += 4) {
+    const int n_c = off[c + 1] - off[c];
+    const uint64_t* sp = src + (size_t)c * seg_cap;
+    for (int i0 = 0; i0 < n_c; i0 += kWave) {
+      const uint64_t cur = i0 + lane < n_c ? sp[i0 + lane] : kPadKey;
+      const uint64_t tail = shfl_u64(list, kWave - 1);
+      const bool keep = cur > tail;
+      const uint64_t mask = __ballot(keep);
+      if (mask == 0) continue;
+      const int pos = n_buf + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+      if (keep) buf[pos] = cur;
+      n_buf += __popcll(mask);
+      __builtin_amdgcn_wave_barrier();
+      if (n_buf >= kWave) {                           // fold 64, keep the rest (< 64) at the front
+        list = fold_group(list, buf[lane]);
+        n_buf -= kWave;
+        const uint64_t rest = lane < n_buf ? buf[kWave + lane] : kPadKey;
+        __builtin_amdgcn_wave_barrier();
+        if (lane < n_buf) buf[lane] = rest;
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
   }
+  if (n_buf > 0) list = fold_group(list, lane < n_buf ? buf[lane] : kPadKey);
   lists[w][lane] = list;
   __syncthreads();
   if (w != 0) return;
@@ -1060,11 +1075,14 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
       p.f_spb *= 2;
     chunking(p.f_q_tiles, N, 512, 64, &p.f_chunk_rows, &p.f_n_chunks);
     // Query-tile groups per XCD: the fewest (of 1, 2, 4, 8) whose tiles take at
-    // most 2 MiB of an XCD's 4 MiB L2 (0: no grouping).
+    // most 3 MiB of an XCD's 4 MiB L2 (0: no grouping). Each history chunk is
+    // then read from HBM by as many XCDs as there are groups (two on the mid
+    // workload; four groups measured no faster and read the store twice as
+    // often).
     p.f_q_groups = 0;
     for (int a = 1; a <= 8; a *= 2) {
       if (p.f_q_tiles % a != 0 || p.f_n_chunks % (8 / a) != 0) continue;
-      if ((size_t)(p.f_q_tiles / a) * ring::kBQ * d * 2 <= ((size_t)2 << 20)) { p.f_q_groups = a; break; }
+      if ((size_t)(p.f_q_tiles / a) * ring::kBQ * d * 2 <= ((size_t)3 << 20)) { p.f_q_groups = a; break; }
     }
     p.seg_cap = 1;                                   // power of two, n_chunks * cap <= 8192
     while (p.seg_cap * 2 * p.f_n_chunks <= 8192) p.seg_cap *= 2;
