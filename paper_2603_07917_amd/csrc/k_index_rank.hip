@@ -351,121 +351,86 @@ __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
   }
 }
 
-// Rank of a small queue (Q <= kRankSmallMax) in one workgroup of 1024
-// threads: the same stable LSD radix sort (8-bit digits, 4 passes), with the
-// keys and request ids kept in registers and scattered through LDS. Element
-// e = 1024 r + t is item r of thread t, so rounds r run in index order. Per
-// pass: digit totals (wave ballots), their exclusive scan, then per round the
-// per-wave digit counts and a stable scatter.
+// Rank of a small queue (Q <= kRankSmallMax) by counting: the position of
+// request i in the stable ascending order is
+//   rank(i) = #{j : key_j < key_i} + #{j < i : key_j == key_i},
+// the same permutation the radix sort gives. Workgroup b owns TI requests
+// i0 = TI b ... and counts over all Q keys, held in LDS: its 16 waves take
+// 64-key chunks in turn, and within a wave S = 64 / TI lane groups take
+// TI-key sub-blocks of each chunk (lane l: request i0 + l % TI, sub-block
+// l / TI). A chunk wholly below i0 counts key_j <= key_i, one wholly past
+// the workgroup's requests counts key_j < key_i, and only the chunk holding
+// them takes the exact rule. Q^2 compares, one compare and one add each:
+// at these sizes a few microseconds spread over the whole chip, where the
+// four-pass radix sort in one workgroup ran serially.
 constexpr int kRankSmallMax = 16384;
-constexpr int kRankSmallThreads = 1024;
-constexpr int kRankSmallItems = kRankSmallMax / kRankSmallThreads;
+constexpr int kRankCountThreads = 1024;
+constexpr int kRankCountWaves = kRankCountThreads / kWave;
 
-__global__ void __launch_bounds__(kRankSmallThreads) rank_small_kernel(const float* __restrict__ g_in, int Q,
+template <int TI>
+__global__ void __launch_bounds__(kRankCountThreads) rank_count_kernel(const float* __restrict__ g_in, int Q,
                                                                        int32_t* __restrict__ order) {
-  constexpr int kWaves = kRankSmallThreads / kWave;
-  __shared__ uint32_t kbuf[kRankSmallMax];
-  __shared__ uint32_t vbuf[kRankSmallMax];
-  __shared__ uint32_t wave_cnt[kWaves][256];
-  __shared__ uint32_t base[256];
-  const int t = threadIdx.x;
+  constexpr int S = kWave / TI;
+  __shared__ __align__(16) uint32_t keys[kRankSmallMax];
+  __shared__ uint32_t part[kRankCountWaves][TI];
+  const int tid = threadIdx.x;
   const int lane = (int)lane_id();
-  const int w = t / kWave;
-  const int rounds = (Q + kRankSmallThreads - 1) / kRankSmallThreads;
-  const uint64_t lt_mask = (1ull << lane) - 1ull;
-  uint32_t key[kRankSmallItems], val[kRankSmallItems];
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);     // wave-uniform: scalar loop control
+  const int n_chunks = (Q + kWave - 1) / kWave;
+  {
+    // All loads in flight at once, then the LDS writes; padding never counts.
+    constexpr int kItems = kRankSmallMax / kRankCountThreads;
+    float g[kItems];
 #pragma unroll
-  for (int r = 0; r < kRankSmallItems; ++r) {
-    const int e = r * kRankSmallThreads + t;
-    key[r] = e < Q ? index_key(g_in[e]) : 0u;
-    val[r] = (uint32_t)e;
+    for (int r = 0; r < kItems; ++r) {
+      const int e = r * kRankCountThreads + tid;
+      g[r] = e < Q ? g_in[e] : 0.0f;
+    }
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+      const int e = r * kRankCountThreads + tid;
+      if (e < n_chunks * kWave) keys[e] = e < Q ? index_key(g[r]) : 0xFFFFFFFFu;
+    }
   }
-  for (int i = t; i < kWaves * 256; i += kRankSmallThreads) (&wave_cnt[0][0])[i] = 0;
   __syncthreads();
-  for (int shift = 0; shift < 32; shift += 8) {
-    // digit totals (wave_cnt is all zero here)
+  const int i0 = blockIdx.x * TI;
+  const int il = lane % TI, sub = lane / TI;
+  const int i = i0 + il;
+  const uint32_t ki = keys[min(i, Q - 1)];
+  const int c_lo = i0 / kWave;                                // chunk holding the requests
+  uint32_t cnt = 0;
+  for (int c = w; c < n_chunks; c += kRankCountWaves) {
+    const int j0 = c * kWave + sub * TI;
+    const uint4* kp = reinterpret_cast<const uint4*>(&keys[j0]);
+    if (c < c_lo) {
 #pragma unroll
-    for (int r = 0; r < kRankSmallItems; ++r) {
-      if (r >= rounds) break;
-      const bool valid = r * kRankSmallThreads + t < Q;
-      const uint32_t digit = (key[r] >> shift) & 255u;
-      uint64_t peers = __ballot(valid);
-#pragma unroll
-      for (int bit = 0; bit < 8; ++bit) {
-        const bool on = (digit >> bit) & 1u;
-        const uint64_t m = __ballot(on);
-        peers &= on ? m : ~m;
+      for (int m = 0; m < TI / 4; ++m) {
+        const uint4 k4 = kp[m];
+        cnt += (k4.x <= ki) + (k4.y <= ki) + (k4.z <= ki) + (k4.w <= ki);
       }
-      if (valid && __popcll(peers & lt_mask) == 0) wave_cnt[w][digit] += (uint32_t)__popcll(peers);
-    }
-    __syncthreads();
-    if (t < 256) {                                     // read and clear column t
-      uint32_t tot = 0;
+    } else if (c > c_lo) {
 #pragma unroll
-      for (int i = 0; i < kWaves; ++i) { tot += wave_cnt[i][t]; wave_cnt[i][t] = 0; }
-      base[t] = tot;
-    }
-    __syncthreads();
-    if (t < kWave) {                                   // exclusive scan of 256 totals, 4 per lane
-      uint32_t c[4], run = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) { c[j] = run; run += base[4 * t + j]; }
-      uint32_t incl = run;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += y;
+      for (int m = 0; m < TI / 4; ++m) {
+        const uint4 k4 = kp[m];
+        cnt += (k4.x < ki) + (k4.y < ki) + (k4.z < ki) + (k4.w < ki);
       }
-      const uint32_t before = incl - run;
+    } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) base[4 * t + j] = before + c[j];
-    }
-    __syncthreads();
-    // stable scatter, round by round
-#pragma unroll
-    for (int r = 0; r < kRankSmallItems; ++r) {
-      if (r >= rounds) break;
-      const bool valid = r * kRankSmallThreads + t < Q;
-      const uint32_t digit = (key[r] >> shift) & 255u;
-      uint64_t peers = __ballot(valid);
-#pragma unroll
-      for (int bit = 0; bit < 8; ++bit) {
-        const bool on = (digit >> bit) & 1u;
-        const uint64_t m = __ballot(on);
-        peers &= on ? m : ~m;
-      }
-      const uint32_t rank_in_wave = (uint32_t)__popcll(peers & lt_mask);
-      if (valid && rank_in_wave == 0) wave_cnt[w][digit] = (uint32_t)__popcll(peers);
-      __syncthreads();
-      if (valid) {
-        uint32_t pos = base[digit] + rank_in_wave;
-        for (int i = 0; i < w; ++i) pos += wave_cnt[i][digit];
-        kbuf[pos] = key[r];
-        vbuf[pos] = val[r];
-      }
-      __syncthreads();
-      if (t < 256) {                                   // advance column t, clear it for the next round
-        uint32_t add = 0;
-#pragma unroll
-        for (int i = 0; i < kWaves; ++i) { add += wave_cnt[i][t]; wave_cnt[i][t] = 0; }
-        base[t] += add;
-      }
-      __syncthreads();
-    }
-#pragma unroll
-    for (int r = 0; r < kRankSmallItems; ++r) {
-      const int e = r * kRankSmallThreads + t;
-      if (e < Q) {
-        key[r] = kbuf[e];
-        val[r] = vbuf[e];
+      for (int m = 0; m < TI; ++m) {
+        const uint32_t kj = keys[j0 + m];
+        cnt += (kj < ki || (kj == ki && j0 + m < i)) ? 1u : 0u;
       }
     }
-    __syncthreads();
   }
 #pragma unroll
-  for (int r = 0; r < kRankSmallItems; ++r) {
-    const int e = r * kRankSmallThreads + t;
-    if (e < Q) order[e] = (int32_t)val[r];
+  for (int o = TI; o < kWave; o <<= 1) cnt += __shfl_xor(cnt, o, kWave);
+  if (sub == 0) part[w][il] = cnt;
+  __syncthreads();
+  if (tid < TI && i < Q) {
+    uint32_t r = 0;
+#pragma unroll
+    for (int ww = 0; ww < kRankCountWaves; ++ww) r += part[ww][tid];
+    order[r] = i;
   }
 }
 
@@ -499,8 +464,15 @@ hipError_t launch_index(const float* mass, const float* cost, const int32_t* pro
 hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipStream_t stream) {
   if (Q == 0) return hipSuccess;
   if (Q <= kRankSmallMax) {
+    // Requests per workgroup: the fewest that still leave >= 256 workgroups
+    // (one per CU), so small queues spread over the chip.
     LaunchScope scope("rank_small", stream);
-    hipLaunchKernelGGL(rank_small_kernel, dim3(1), dim3(kRankSmallThreads), 0, stream, index, Q, order);
+    if (Q <= 4096)
+      hipLaunchKernelGGL(rank_count_kernel<16>, dim3((Q + 15) / 16), dim3(kRankCountThreads), 0, stream, index, Q, order);
+    else if (Q <= 8192)
+      hipLaunchKernelGGL(rank_count_kernel<32>, dim3((Q + 31) / 32), dim3(kRankCountThreads), 0, stream, index, Q, order);
+    else
+      hipLaunchKernelGGL(rank_count_kernel<64>, dim3((Q + 63) / 64), dim3(kRankCountThreads), 0, stream, index, Q, order);
     return hipGetLastError();
   }
   const int n_tiles = (Q + kRankTile - 1) / kRankTile;

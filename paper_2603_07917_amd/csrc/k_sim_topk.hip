@@ -309,21 +309,20 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     for (int t = 0; t < NQT; ++t) {
       const int ql = 32 * t + l32;
       thr[t] = fmaxf(float_below(sm.theta0[ql]), sm.theta[ql]);
+      // Bit i = [s_i > thr] is the sign bit of thr - s_i, shifted in with
+      // one funnel shift per score.
       uint32_t m = 0;
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
+      for (int u = 1; u >= 0; --u)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) m |= (acc[u][t][v] > thr[t] ? 1u : 0u) << (16 * u + v);
+        for (int v = 15; v >= 0; --v)
+          m = __builtin_amdgcn_alignbit(m, __float_as_uint(thr[t] - acc[u][t][v]), 31);
       if (!full_step) {
-        uint32_t valid = 0;
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int h = h0 + 64 * w + 32 * u + 8 * (v >> 2) + 4 * half + (v & 3);
-            valid |= (h < step_end ? 1u : 0u) << (16 * u + v);
-          }
-        m &= valid;
+        // Bit i = 16 u + v is row h0 + 64 w + 4 half + 8 (i / 4) + i % 4:
+        // rows grow with i, so the rows inside the step are the lowest bits.
+        const int c = min(max(step_end - h0 - 64 * w - 4 * half, 0), 64);
+        const int n_in = 4 * (c >> 3) + min(c & 7, 4);
+        m &= n_in >= 32 ? ~0u : (1u << n_in) - 1u;
       }
       if (q0 + ql >= Q) m = 0;
       bits[t] = m;
@@ -858,11 +857,11 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
       const uint32_t lo = mk[0] | (mk[1] << 16), hi = mk[2] | (mk[3] << 16);
       uint64_t m = ((uint64_t)hi << 32) | lo;
       if (step_end - h0 < kStepRows) {                          // last, partial step
-        uint64_t valid = 0;
-#pragma unroll
-        for (int i = 0; i < 64; ++i)
-          valid |= (uint64_t)(32 * (i >> 4) + 8 * ((i >> 2) & 3) + (i & 3) < lim ? 1u : 0u) << i;
-        m &= valid;
+        // r(i) grows with i, so the rows inside the step are the lowest
+        // bits: bits 4g..4g+3 are rows 8g..8g+3, hence the count below.
+        const int c = min(max(lim, 0), 128);
+        const int n_in = 4 * (c >> 3) + min(c & 7, 4);
+        m &= n_in >= 64 ? ~0ull : (1ull << n_in) - 1ull;
       }
       if (m == 0) continue;
       const int ql = 128 * wq + 32 * t + l32;

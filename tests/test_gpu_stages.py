@@ -101,7 +101,8 @@ def test_index_config4_full():
 
 
 # ------------------------------------------------------------------ rank
-@pytest.mark.parametrize("Q", [1, 2, 3, 2047, 2048, 2049, 5000, 16384, 16385, 65536, 131073])
+@pytest.mark.parametrize("Q", [1, 2, 3, 63, 64, 65, 2047, 2048, 2049, 4096, 4097, 5000, 8192, 8193,
+                               16383, 16384, 16385, 65536, 131073])
 def test_rank_bit_exact(Q):
     rng = np.random.default_rng(Q)
     g = np.round(rng.uniform(0, 50, size=Q)).astype(np.float32)   # many exact ties
@@ -111,6 +112,13 @@ def test_rank_bit_exact(Q):
     parity.check_rank(order, g)
     h = rng.lognormal(8, 3, size=Q).astype(np.float32)            # wide dynamic range
     parity.check_rank(host(sage.rank(dev(h))), h)
+
+
+@pytest.mark.parametrize("Q", [100, 4096, 8000, 16384, 20000])
+def test_rank_all_equal_is_identity(Q):
+    # every key tied: the stable order is the request order itself
+    order = host(sage.rank(dev(np.full(Q, 7.0, dtype=np.float32))))
+    assert np.array_equal(order, np.arange(Q, dtype=np.int32))
 
 
 def test_rank_negative_and_signed_zero():
