@@ -161,8 +161,7 @@ __device__ uint64_t merge_into_list(uint64_t* list, const uint64_t* buf, int n_b
 #pragma unroll
   for (int s = 0; s < S; ++s) lv[s] = list[s * 64 + lane];
   uint64_t b = lane < n_buf ? buf[lane] : kPadKey;
-  b = wave_sort_desc64(b);
-  const uint64_t br = shfl_u64(b, 63 - lane);         // ascending along the lanes
+  const uint64_t br = wave_sort64(b, false);          // ascending along the lanes
   lv[S - 1] = umax64(lv[S - 1], br);                  // bitonic over the KL positions
 #pragma unroll
   for (int st = S / 2; st >= 1; st >>= 1) {
@@ -185,7 +184,7 @@ __device__ uint64_t merge_into_list(uint64_t* list, const uint64_t* buf, int n_b
   uint64_t sel = lv[0];
 #pragma unroll
   for (int s = 1; s < S; ++s) if (s == ks) sel = lv[s];
-  return shfl_u64(sel, kl);
+  return lane_value_u64(sel, kl);
 }
 
 // ------------------------------------------------------------------------
@@ -419,10 +418,9 @@ __device__ __forceinline__ uint64_t wave_bitonic_clean_desc64(uint64_t v) {
 // its 64 largest keys: skipped when no key beats the list's last one,
 // otherwise a wave bitonic sort, C_i = max(A_i, B_{63-i}) and half-cleaners.
 __device__ __forceinline__ uint64_t fold_group(uint64_t list, uint64_t key) {
-  if (!__any(key > shfl_u64(list, kWave - 1))) return list;
-  key = wave_sort_desc64(key);
-  const uint64_t rev = shfl_u64(key, kWave - 1 - (int)lane_id());
-  return wave_bitonic_clean_desc64(list > rev ? list : rev);
+  if (!__any(key > lane_value_u64(list, kWave - 1))) return list;
+  const uint64_t asc = wave_sort64(key, false);       // B_{63-i} of the descending order
+  return wave_bitonic_clean_desc64(list > asc ? list : asc);
 }
 
 // Wave 0 folds the lists of waves 1..3 (in LDS) into its own.
@@ -939,27 +937,53 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
   uint64_t* buf = pend[w];
   uint64_t list = kPadKey;
   int n_buf = 0;                                      // keys waiting in buf (wave-uniform, < 64)
-  for (int c = w; c < n_chunks; c += 4) {
-    const int n_c = off[c + 1] - off[c];
-    const uint64_t* sp = src + (size_t)c * seg_cap;
-    for (int i0 = 0; i0 < n_c; i0 += kWave) {
-      const uint64_t cur = i0 + lane < n_c ? sp[i0 + lane] : kPadKey;
-      const uint64_t tail = shfl_u64(list, kWave - 1);
-      const bool keep = cur > tail;
-      const uint64_t mask = __ballot(keep);
-      if (mask == 0) continue;
-      const int pos = n_buf + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-      if (keep) buf[pos] = cur;
-      n_buf += __popcll(mask);
+  auto take = [&](uint64_t cur) {
+    const uint64_t tail = lane_value_u64(list, kWave - 1);
+    const bool keep = cur > tail;
+    const uint64_t mask = __ballot(keep);
+    if (mask == 0) return;
+    const int pos = n_buf + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+    if (keep) buf[pos] = cur;
+    n_buf += __popcll(mask);
+    __builtin_amdgcn_wave_barrier();
+    if (n_buf >= kWave) {                             // fold 64, keep the rest (< 64) at the front
+      list = fold_group(list, buf[lane]);
+      n_buf -= kWave;
+      const uint64_t rest = lane < n_buf ? buf[kWave + lane] : kPadKey;
       __builtin_amdgcn_wave_barrier();
-      if (n_buf >= kWave) {                           // fold 64, keep the rest (< 64) at the front
-        list = fold_group(list, buf[lane]);
-        n_buf -= kWave;
-        const uint64_t rest = lane < n_buf ? buf[kWave + lane] : kPadKey;
-        __builtin_amdgcn_wave_barrier();
-        if (lane < n_buf) buf[lane] = rest;
-        __builtin_amdgcn_wave_barrier();
+      if (lane < n_buf) buf[lane] = rest;
+      __builtin_amdgcn_wave_barrier();
+    }
+  };
+  // The first 64 keys of kPre segments are loaded at once (segments hold
+  // about a thousand keys / n_chunks, mostly fewer than 64), then consumed
+  // in order; longer segments finish with further loads.
+  constexpr int kPre = 8;
+  for (int cb = w; cb < n_chunks; cb += 4 * kPre) {
+    uint64_t cur[kPre];
+    int n_c[kPre];
+#pragma unroll
+    for (int j = 0; j < kPre; ++j) {
+      const int c = cb + 4 * j;
+      n_c[j] = c < n_chunks ? off[c + 1] - off[c] : 0;
+      cur[j] = lane < n_c[j] ? src[(size_t)c * seg_cap + lane] : kPadKey;
+    }
+    // One copy of the consuming code: the registers shift down each turn.
+#pragma unroll 1
+    for (int j = 0; j < kPre; ++j) {
+      uint64_t x = cur[0];
+      const int nx = n_c[0];
+#pragma unroll
+      for (int i = 0; i + 1 < kPre; ++i) {
+        cur[i] = cur[i + 1];
+        n_c[i] = n_c[i + 1];
+      }
+      const uint64_t* sp = src + (size_t)(cb + 4 * j) * seg_cap;
+      for (int i0 = kWave;; i0 += kWave) {
+        take(x);
+        if (i0 >= nx) break;
+        x = i0 + lane < nx ? sp[i0 + lane] : kPadKey;
       }
     }
   }

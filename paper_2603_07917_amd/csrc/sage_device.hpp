@@ -40,7 +40,8 @@ __device__ __forceinline__ float key_sim(uint64_t k) { return f32_from_order_bit
 __device__ __forceinline__ int32_t key_id(uint64_t k) { return (int32_t)(~(uint32_t)k); }
 
 // ---------------------------------------------------------------------------
-// Cross-lane moves within a 64-wide wavefront (ds_bpermute based).
+// Cross-lane moves within a 64-wide wavefront: ds_bpermute for a lane chosen
+// at run time, DPP and the lane-swap instructions for fixed strides.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
 
@@ -50,36 +51,80 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src_lane) {
   hi = (uint32_t)__shfl((int)hi, src_lane, kWave);
   return ((uint64_t)hi << 32) | lo;
 }
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
-  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-  lo = (uint32_t)__shfl_xor((int)lo, mask, kWave);
-  hi = (uint32_t)__shfl_xor((int)hi, mask, kWave);
+
+// Value held by lane (lane ^ S), for a stride S fixed at compile time, with
+// no LDS round trip: DPP within a row of 16 lanes (S = 1, 2: quad
+// permutes; S = 4: row half-mirror then quad reverse, i -> 7 - i -> i ^ 4;
+// S = 8: row rotate by 8), and the lane-swap instructions across rows
+// (S = 16, 32). permlane16_swap on two copies of v leaves v[lane - 16] in
+// the first copy's odd rows and v[lane + 16] in the second copy's even rows;
+// permlane32_swap does the same for the two halves of the wave.
+template <int S>
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t v) {
+  if constexpr (S == 1) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+  } else if constexpr (S == 2) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
+  } else if constexpr (S == 4) {
+    const int t = __builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, false);
+    return (uint32_t)__builtin_amdgcn_mov_dpp(t, 0x1B, 0xF, 0xF, false);
+  } else if constexpr (S == 8) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);
+  } else if constexpr (S == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return (__lane_id() & 16) ? r[0] : r[1];
+  } else {
+    static_assert(S == 32, "stride must be a power of two below 64");
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return (__lane_id() & 32) ? r[0] : r[1];
+  }
+}
+template <int S>
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t v) {
+  const uint32_t lo = xor_lane_u32<S>((uint32_t)v), hi = xor_lane_u32<S>((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+// The same for a stride known only after unrolling (folds to one case).
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t v, int stride) {
+  switch (stride) {
+    case 1: return xor_lane_u64<1>(v);
+    case 2: return xor_lane_u64<2>(v);
+    case 4: return xor_lane_u64<4>(v);
+    case 8: return xor_lane_u64<8>(v);
+    case 16: return xor_lane_u64<16>(v);
+    default: return xor_lane_u64<32>(v);
+  }
+}
+
+// Key of a fixed lane, in every lane.
+__device__ __forceinline__ uint64_t lane_value_u64(uint64_t v, int src_lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src_lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), src_lane);
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Compare-exchange with the lane `stride` away: the lane whose `stride` bit
-// is clear keeps the larger key when `desc`, the smaller one otherwise.
+// Compare-exchange with the lane `stride` away (stride a power of two below
+// 64): the lane whose `stride` bit is clear keeps the larger key when
+// `desc`, the smaller one otherwise.
 __device__ __forceinline__ uint64_t cx_lanes(uint64_t v, int stride, bool desc) {
-  uint64_t o = shfl_xor_u64(v, stride);
-  bool low = (lane_id() & stride) == 0;
-  bool keep_max = (low == desc);
-  uint64_t mx = v > o ? v : o;
-  uint64_t mn = v > o ? o : v;
-  return keep_max ? mx : mn;
+  const uint64_t o = xor_lane_u64(v, stride);
+  const bool keep_max = ((lane_id() & stride) == 0) == desc;
+  return ((v > o) == keep_max) ? v : o;
 }
 
-// Sort the wave's 64 keys (one per lane) into descending order across lanes
-// (lane 0 holds the largest): bitonic sorting network.
-__device__ __forceinline__ uint64_t wave_sort_desc64(uint64_t v) {
+// Sort the wave's 64 keys (one per lane) across lanes with a bitonic
+// sorting network: descending (lane 0 holds the largest) or ascending.
+__device__ __forceinline__ uint64_t wave_sort64(uint64_t v, bool descending) {
   const int lane = (int)lane_id();
 #pragma unroll
   for (int size = 2; size <= 64; size <<= 1) {
-    const bool desc_block = (lane & size) == 0;   // always true at size 64
+    const bool desc_block = ((lane & size) == 0) == descending;   // the whole wave at size 64
 #pragma unroll
     for (int stride = size >> 1; stride > 0; stride >>= 1) v = cx_lanes(v, stride, desc_block);
   }
   return v;
 }
+__device__ __forceinline__ uint64_t wave_sort_desc64(uint64_t v) { return wave_sort64(v, true); }
 
 // ---------------------------------------------------------------------------
 // Wave reductions / scans.
