@@ -32,12 +32,6 @@
 namespace sage {
 namespace {
 
-typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
-
-// Address of element (r, c) of an embedding matrix in either layout.
-__device__ __forceinline__ const uint16_t* emb_at(const EmbView& m, int r, int c) {
-  return m.base + (long long)(c >> 5) * m.panel + (long long)r * m.row + (c & 31);
-}
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 
 constexpr int kThreads = 256;
@@ -448,7 +442,7 @@ __device__ __forceinline__ uint64_t fold_lists(uint64_t list, const uint64_t (&l
 // the chip idle and each wave latency-bound).
 template <int VPL, int WAVES>
 __global__ void __launch_bounds__(256 * (WAVES > 1 ? WAVES / 4 : 1)) threshold_select_kernel(
-    const float* __restrict__ gm, int Q, int m, int k, float* __restrict__ theta0) {
+    const float* __restrict__ gm, int Q, int m, int k, float* __restrict__ theta0, int* __restrict__ clear) {
   __shared__ uint32_t part[2][WAVES > 1 ? WAVES : 1];
   __shared__ uint32_t ext[2][WAVES > 1 ? WAVES : 1];
   const int lane = (int)lane_id();
@@ -493,7 +487,10 @@ __global__ void __launch_bounds__(256 * (WAVES > 1 ? WAVES / 4 : 1)) threshold_s
     }
     if (n >= (uint32_t)k) T = c;
   }
-  if (lane == 0 && (WAVES == 1 || w == 0)) theta0[q] = k <= m ? f32_from_order_bits(T) : -__builtin_inff();
+  if (lane == 0 && (WAVES == 1 || w == 0)) {
+    theta0[q] = k <= m ? f32_from_order_bits(T) : -__builtin_inff();
+    if (clear) clear[q] = 0;                            // the next kernel's per-query counter
+  }
 }
 // ========================================================================
 // Filtered path for k <= 64.
@@ -1011,7 +1008,7 @@ hipError_t launch_lists(EmbView queries, int Q, EmbView hist, int N, int d, int 
 
 hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int k,
                         const SimTopkPlan& p, int q_tiles, bool big, float* gm, float* theta0,
-                        hipStream_t stream) {
+                        int* clear, hipStream_t stream) {
   {
     LaunchScope scope("threshold_sample", stream);
     const dim3 grid(q_tiles, p.n_samples);
@@ -1020,7 +1017,7 @@ hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int 
       const dim3 rgrid(q_tiles, (p.n_samples + spb - 1) / spb);
       hipLaunchKernelGGL(threshold_sample_ring_kernel, rgrid, dim3(kThreads), 0, stream, queries, Q,
                          hist, N, d, p.sample_every, p.n_samples, spb, gm);
-    } else if (p.list_len == 128) {
+    } else if (p.list_len == 128 && !p.stream) {
       hipLaunchKernelGGL((threshold_sample_kernel<2>), grid, dim3(kThreads), 0, stream, queries, Q,
                          hist, N, d, p.sample_every, p.n_samples, gm);
     } else {
@@ -1032,19 +1029,19 @@ hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int 
   LaunchScope scope("threshold_select", stream);
   if (Q < 512) {                                       // one 16-wave workgroup per query
     if (m <= 2 * 16 * kWave)
-      hipLaunchKernelGGL((threshold_select_kernel<2, 16>), dim3(Q), dim3(1024), 0, stream, gm, Q, m, k, theta0);
+      hipLaunchKernelGGL((threshold_select_kernel<2, 16>), dim3(Q), dim3(1024), 0, stream, gm, Q, m, k, theta0, clear);
     else
-      hipLaunchKernelGGL((threshold_select_kernel<8, 16>), dim3(Q), dim3(1024), 0, stream, gm, Q, m, k, theta0);
+      hipLaunchKernelGGL((threshold_select_kernel<8, 16>), dim3(Q), dim3(1024), 0, stream, gm, Q, m, k, theta0, clear);
   } else {                                             // four queries (wavefronts) per workgroup
     const dim3 grid((Q + 3) / 4);
     if (m <= 16 * kWave)
-      hipLaunchKernelGGL((threshold_select_kernel<16, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+      hipLaunchKernelGGL((threshold_select_kernel<16, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0, clear);
     else if (m <= 32 * kWave)
-      hipLaunchKernelGGL((threshold_select_kernel<32, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+      hipLaunchKernelGGL((threshold_select_kernel<32, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0, clear);
     else if (m <= 64 * kWave)
-      hipLaunchKernelGGL((threshold_select_kernel<64, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+      hipLaunchKernelGGL((threshold_select_kernel<64, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0, clear);
     else
-      hipLaunchKernelGGL((threshold_select_kernel<128, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0);
+      hipLaunchKernelGGL((threshold_select_kernel<128, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0, clear);
   }
   return hipGetLastError();
 }
@@ -1110,6 +1107,18 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
     p.seg_cap = 1;                                   // power of two, n_chunks * cap <= 8192
     while (p.seg_cap * 2 * p.f_n_chunks <= 8192) p.seg_cap *= 2;
   }
+  // Few queries against a large store: the stream path (one pass over the
+  // store, bound by HBM), given a threshold pre-pass. About k * SR keys
+  // beat theta0 per query; the array holds four times that.
+  p.stream = Q <= kStreamMaxQ && d <= kStreamMaxD && k <= 256 && p.n_samples > 0;
+  if (p.stream) {
+    p.fast = false;
+    long rows = ((long)N + 511) / 512;                   // about two workgroups per CU
+    rows = (rows + 63) / 64 * 64;
+    p.s_chunk_rows = (int)rows;
+    p.s_cap = 4096;
+    while (p.s_cap < 4L * k * p.sample_every) p.s_cap *= 2;
+  }
   size_t o = 0;
   p.off_partial = o; o = align256(o + (size_t)Q * p.n_chunks * L * sizeof(uint64_t));
   const int groups = merge_groups(Q, p.n_chunks, L);
@@ -1119,6 +1128,11 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   if (p.fast) {
     p.off_seg = o;    o = align256(o + (size_t)Q * p.f_n_chunks * p.seg_cap * sizeof(uint64_t));
     p.off_segcnt = o; o = align256(o + (size_t)Q * p.f_n_chunks * sizeof(int));
+    p.off_flags = o;  o = align256(o + (size_t)Q * sizeof(int));
+  }
+  if (p.stream) {
+    p.off_cand = o;   o = align256(o + (size_t)Q * p.s_cap * sizeof(uint64_t));
+    p.off_ccount = o; o = align256(o + (size_t)Q * sizeof(int));
     p.off_flags = o;  o = align256(o + (size_t)Q * sizeof(int));
   }
   p.total_bytes = o;
@@ -1137,7 +1151,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
   hipError_t e;
   if (p.fast) {
     if (p.n_samples > 0) {
-      e = launch_theta(queries, Q, hist, N, d, k, p, p.f_q_tiles, true, gm, theta0, stream);
+      e = launch_theta(queries, Q, hist, N, d, k, p, p.f_q_tiles, true, gm, theta0, nullptr, stream);
       if (e != hipSuccess) return e;
     }
     uint64_t* seg = reinterpret_cast<uint64_t*>(ws + p.off_seg);
@@ -1159,8 +1173,24 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     if (e != hipSuccess) return e;
     return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, merge_lists, ids, sims, stream);
   }
+  if (p.stream) {
+    uint64_t* cand = reinterpret_cast<uint64_t*>(ws + p.off_cand);
+    int* ccount = reinterpret_cast<int*>(ws + p.off_ccount);
+    int* flags = reinterpret_cast<int*>(ws + p.off_flags);
+    e = launch_theta(queries, Q, hist, N, d, k, p, 1, false, gm, theta0, ccount, stream);
+    if (e != hipSuccess) return e;
+    e = launch_stream_search(queries, Q, hist, N, d, k, p.s_chunk_rows, theta0, p.s_cap, cand, ccount, flags,
+                             ids, sims, stream);
+    if (e != hipSuccess) return e;
+    // Exact fallback for queries whose candidates overflowed (no work otherwise).
+    if (p.list_len == 64) e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
+    else if (p.list_len == 128) e = launch_lists<2, 128>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
+    else e = launch_lists<1, 256>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
+    if (e != hipSuccess) return e;
+    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, merge_lists, ids, sims, stream);
+  }
   if (p.n_samples > 0) {
-    e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, false, gm, theta0, stream);
+    e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, false, gm, theta0, nullptr, stream);
     if (e != hipSuccess) return e;
   }
   const float* th = p.n_samples > 0 ? theta0 : nullptr;

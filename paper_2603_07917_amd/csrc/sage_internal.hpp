@@ -31,6 +31,11 @@ struct EmbView {
 };
 inline EmbView rows_view(const uint16_t* base, int d) { return EmbView{base, 32, (long long)d}; }
 inline EmbView panels_view(const uint16_t* base, int rows) { return EmbView{base, 32LL * rows, 32}; }
+// Address of element (r, c) of an embedding matrix in either layout.
+__device__ __forceinline__ const uint16_t* emb_at(const EmbView& m, int r, int c) {
+  return m.base + (long long)(c >> 5) * m.panel + (long long)r * m.row + (c & 31);
+}
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 
 // Launch plan of the neighbour search (threshold pre-pass, search, merge).
 struct SimTopkPlan {
@@ -49,11 +54,22 @@ struct SimTopkPlan {
   int f_spb;        // sampled steps per threshold-sampling workgroup
   int f_q_groups;   // query-tile groups across the 8 XCDs (0: plain mapping)
   int seg_cap;      // candidate keys per (query, chunk) segment
+  // few-query stream path (Q <= kStreamMaxQ, any k <= 256)
+  bool stream;
+  int s_chunk_rows; // history rows per workgroup
+  int s_cap;        // candidate keys per query
   // workspace layout (byte offsets, 256-aligned)
-  size_t off_partial, off_merge, off_gm, off_theta, off_seg, off_segcnt, off_flags, total_bytes;
+  size_t off_partial, off_merge, off_gm, off_theta, off_seg, off_segcnt, off_flags, off_cand, off_ccount,
+      total_bytes;
   size_t workspace_bytes() const { return total_bytes; }
 };
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
+// Few-query stream path: limits, and the search + candidate select.
+constexpr int kStreamMaxQ = 16;
+constexpr int kStreamMaxD = 2048;
+hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int d, int k, int chunk_rows,
+                                const float* theta0, int cap, uint64_t* cand, int* cand_count, int* flags,
+                                int32_t* ids, float* sims, hipStream_t stream);
 
 // Launchers: each enqueues kernels on `stream` and returns the HIP status of
 // the launch (hipSuccess or the first error).

@@ -59,6 +59,13 @@ CASES = [
     (3, 10, 64, 32, 16),        # N < k: padded with -1 / -inf
     (8, 300000, 64, 128, 512),  # few queries, hundreds of chunk lists: two-level merge
     (8, 200000, 32, 200, 64),
+    # few queries (at most 16): the stream search over the store
+    (1, 50001, 768, 64, 256),
+    (16, 70000, 96, 256, 64),
+    (7, 33333, 2048, 100, 128),
+    (16, 20000, 64, 1, 16),
+    (9, 65536, 32, 64, 32),
+    (4, 40000, 2080, 32, 64),   # d above the stream path's limit: the list path
 ]
 
 
