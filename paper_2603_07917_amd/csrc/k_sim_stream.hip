@@ -39,7 +39,7 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast
 __global__ void __launch_bounds__(kThreads) sim_stream_kernel(
     EmbView queries, int Q, EmbView hist, int N, int d, int chunk_rows, const float* __restrict__ theta0,
     int cap, uint64_t* __restrict__ cand, int* __restrict__ cand_count) {
-  __shared__ __align__(16) uint4 qfrag[kStreamMaxD / 32 * kWave];
+  extern __shared__ uint4 qfrag[];                  // d / 32 KiB, sized at launch
   __shared__ uint64_t lbuf[kStreamMaxQ][kLCap];
   __shared__ int lcnt[kStreamMaxQ];
   __shared__ int gbase[kStreamMaxQ];
@@ -286,7 +286,8 @@ hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int
   {
     LaunchScope scope("sim_topk", stream);
     const int blocks = (N + chunk_rows - 1) / chunk_rows;
-    hipLaunchKernelGGL(sim_stream_kernel, dim3(blocks), dim3(kThreads), 0, stream, queries, Q, hist, N, d,
+    const size_t lds = (size_t)(d / 32) * kWave * sizeof(uint4);   // sized to d: more workgroups per CU
+    hipLaunchKernelGGL(sim_stream_kernel, dim3(blocks), dim3(kThreads), lds, stream, queries, Q, hist, N, d,
                        chunk_rows, theta0, cap, cand, cand_count);
   }
   LaunchScope scope("topk_select", stream);
