@@ -94,8 +94,11 @@ def stage_rooflines(stages, rows_per_launch: float, d: int, k: int, B: int):
     return out
 
 
-def kernel_name(k: int) -> str:
-    """The kernel behind the `sim_topk` timer label: the filtered path for k <= 64."""
+def kernel_name(k: int, Q: int = 1 << 30) -> str:
+    """The kernel behind the `sim_topk` timer label: the stream search for at
+    most 16 queries (large stores), else the filtered path for k <= 64."""
+    if Q <= 16:
+        return "sim_stream_kernel"
     return "sim_filter_kernel" if k <= 64 else "sim_topk_kernel"
 
 
@@ -385,7 +388,7 @@ def run_streaming(args, torch, sage, workloads):
                    "tau": spec.tau, "seed": [workloads.SEED_BASE, 5]},
         "latency_ms": {"p50": float(np.percentile(lat, 50)), "p99": float(np.percentile(lat, 99))},
         "reindexed_rows_per_s": queue.slots * args.steps / elapsed,
-        "roofline": {"bound": "hbm", "kernel": kernel_name(spec.k), "achieved": achieved,
+        "roofline": {"bound": "hbm", "kernel": kernel_name(spec.k, batch), "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None, "avg_launch_us": k1_avg_s * 1e6, "bytes_per_launch": k1_bytes},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},

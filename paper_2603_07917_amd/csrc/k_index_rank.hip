@@ -271,35 +271,42 @@ __global__ void __launch_bounds__(kRankThreads) rank_hist_kernel(const float* __
 }
 
 // Exclusive scan of n entries in one workgroup of 1024 threads.
-__global__ void __launch_bounds__(1024) rank_scan_kernel(uint32_t* __restrict__ a, int n) {
-  __shared__ uint32_t part[1024];
+// Per-digit exclusive scan over the tiles: workgroup d scans hist[d][0..n_tiles)
+// in place (contiguous, 256 counts per turn) and leaves the digit's total in
+// total[d]. The scatter adds the exclusive scan of the 256 totals.
+__global__ void __launch_bounds__(256) rank_scan_kernel(uint32_t* __restrict__ hist, int n_tiles,
+                                                        uint32_t* __restrict__ total) {
+  __shared__ uint32_t wsum[4];
   const int t = threadIdx.x;
-  const int per = (n + 1023) / 1024;
-  const int s = t * per;
-  const int e = min(n, s + per);
-  uint32_t sum = 0;
-  for (int i = s; i < e; ++i) sum += a[i];
-  part[t] = sum;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    uint32_t v = t >= off ? part[t - off] : 0u;
+  const int lane = (int)lane_id();
+  const int w = t / kWave;
+  uint32_t* row = hist + (size_t)blockIdx.x * n_tiles;
+  uint32_t carry = 0;
+  for (int base = 0; base < n_tiles; base += 256) {
+    const int i = base + t;
+    const uint32_t v = i < n_tiles ? row[i] : 0u;
+    uint32_t incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t y = (uint32_t)__shfl_up((int)incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    if (lane == kWave - 1) wsum[w] = incl;
     __syncthreads();
-    part[t] += v;
+    uint32_t before = carry;
+    for (int ww = 0; ww < w; ++ww) before += wsum[ww];
+    if (i < n_tiles) row[i] = before + incl - v;
+    carry += wsum[0] + wsum[1] + wsum[2] + wsum[3];
     __syncthreads();
   }
-  uint32_t run = part[t] - sum;
-  for (int i = s; i < e; ++i) {
-    const uint32_t v = a[i];
-    a[i] = run;
-    run += v;
-  }
+  if (t == 0) total[blockIdx.x] = carry;
 }
 
 __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
     const float* __restrict__ g_in, const uint32_t* __restrict__ k_in,
     const uint32_t* __restrict__ v_in, int Q, int shift, int n_tiles,
-    const uint32_t* __restrict__ offsets, uint32_t* __restrict__ k_out,
-    uint32_t* __restrict__ v_out) {
+    const uint32_t* __restrict__ offsets, const uint32_t* __restrict__ digit_total,
+    uint32_t* __restrict__ k_out, uint32_t* __restrict__ v_out) {
   constexpr int kWaves = kRankThreads / kWave;
   __shared__ uint32_t base_off[256];
   __shared__ uint32_t running[256];
@@ -307,7 +314,23 @@ __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
   const int t = threadIdx.x;
   const int lane = (int)lane_id();
   const int w = t / kWave;
-  base_off[t] = offsets[t * n_tiles + blockIdx.x];
+  {
+    // exclusive scan of the 256 digit totals (one per thread), plus this
+    // tile's offset within the digit
+    const uint32_t v = digit_total[t];
+    uint32_t incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t y = (uint32_t)__shfl_up((int)incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    if (lane == kWave - 1) running[w] = incl;           // wave totals (running is reset below)
+    __syncthreads();
+    uint32_t before = 0;
+    for (int ww = 0; ww < w; ++ww) before += running[ww];
+    base_off[t] = before + incl - v + offsets[t * n_tiles + blockIdx.x];
+    __syncthreads();
+  }
   running[t] = 0;
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) wave_cnt[i][t] = 0;
@@ -439,7 +462,7 @@ __global__ void __launch_bounds__(kRankCountThreads) rank_count_kernel(const flo
 size_t rank_workspace_bytes(int Q) {
   if (Q <= 0) return 0;
   const size_t tiles = ((size_t)Q + kRankTile - 1) / kRankTile;
-  return 4 * (size_t)Q * sizeof(uint32_t) + 256 * tiles * sizeof(uint32_t) + 256;
+  return 4 * (size_t)Q * sizeof(uint32_t) + 256 * (tiles + 1) * sizeof(uint32_t) + 256;
 }
 
 hipError_t launch_index(const float* mass, const float* cost, const int32_t* prompt_len,
@@ -481,6 +504,7 @@ hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipS
   uint32_t* kB = vA + Q;
   uint32_t* vB = kB + Q;
   uint32_t* hist = vB + Q;
+  uint32_t* totals = hist + 256 * (size_t)n_tiles;
   const uint32_t* k_in = nullptr;
   const uint32_t* v_in = nullptr;
   for (int pass = 0; pass < 4; ++pass) {
@@ -495,12 +519,12 @@ hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipS
     }
     {
       LaunchScope scope("rank_scan", stream);
-      hipLaunchKernelGGL(rank_scan_kernel, dim3(1), dim3(1024), 0, stream, hist, 256 * n_tiles);
+      hipLaunchKernelGGL(rank_scan_kernel, dim3(256), dim3(256), 0, stream, hist, n_tiles, totals);
     }
     {
       LaunchScope scope("rank_scatter", stream);
       hipLaunchKernelGGL(rank_scatter_kernel, dim3(n_tiles), dim3(kRankThreads), 0, stream, index,
-                         k_in, v_in, Q, shift, n_tiles, hist, k_out, v_out);
+                         k_in, v_in, Q, shift, n_tiles, hist, totals, k_out, v_out);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
