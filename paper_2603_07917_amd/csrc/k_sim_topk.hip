@@ -695,6 +695,10 @@ __device__ __forceinline__ void sweep(const EmbView& hist, int N, int h_first, i
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      // The half's last eight MFMAs stay before the barrier (left alone, the
+      // compiler sinks seven of them past it), so the matrix pipe has work
+      // queued while the wave waits for its reads and for the other waves.
+      __builtin_amdgcn_sched_barrier(0);
       if (steady) {
         wait_loads<kLoads + kLoads / 2>();
       } else {
