@@ -105,6 +105,32 @@ int sage_store_insert(const float* emb, const int32_t* out_len, int n, int d, lo
                       int capacity, uint16_t* ring_emb, int32_t* ring_len, sage_stream_t stream);
 
 /*
+ * sage_queue_admit / sage_queue_dispatch - per-decision bookkeeping of a
+ * standing queue of `slots` pending requests (Sec. 3.3: the queue is
+ * re-ranked at every scheduling decision; each decision admits `batch` new
+ * arrivals into the slots the previous one freed and dispatches `batch`).
+ *   admit: new request i takes slot free_slots[i]: mass[s, :] = new_mass[i, :],
+ *          plen[s] = new_plen[i], request[s] = next_request + i. Slots
+ *          outside [0, slots) are skipped (device data, not checked on the
+ *          host).
+ *          free_slots [batch] int64, new_mass [batch, B] f32, new_plen [batch]
+ *          int32 in; mass [slots, B] f32, plen [slots] int32, request [slots]
+ *          int64 updated.
+ *   dispatch: the first `batch` entries of order (a sage_rank result over
+ *          the slots) leave: free_slots[i] = order[i], dispatched[i] =
+ *          request[order[i]] (-1 for an entry outside [0, slots)).
+ *          order [slots] int32, request [slots] int64 in; free_slots [batch],
+ *          dispatched [batch] int64 out.
+ * SAGE_EINVAL: batch < 0, slots < batch, B outside [1, SAGE_MAX_BINS],
+ * next_request < 0, NULL or misaligned pointer (when batch > 0).
+ */
+int sage_queue_admit(const int64_t* free_slots, int batch, const float* new_mass, const int32_t* new_plen,
+                     int B, long long next_request, int slots, float* mass, int32_t* plen, int64_t* request,
+                     sage_stream_t stream);
+int sage_queue_dispatch(const int32_t* order, int batch, const int64_t* request, int slots,
+                        int64_t* free_slots, int64_t* dispatched, sage_stream_t stream);
+
+/*
  * sage_predict_workspace_bytes - bytes of device workspace sage_predict needs
  * for these sizes (holds the per-stream partial neighbour lists). Returns 0
  * for invalid sizes.

@@ -144,6 +144,35 @@ dim3 panels_grid(int rows, int d) {
   while ((long)gx * gy > 8192 && gx > 1) gx = (gx + 1) / 2;
   return dim3(gx, gy);
 }
+// Standing queue of the streaming scheduler (Sec. 3.3: the queue is
+// re-ranked at every decision). Admit: new request i takes slot free[i]: its
+// predicted masses, prompt length and arrival number. Slots outside
+// [0, slots) are skipped.
+__global__ void queue_admit_kernel(const int64_t* __restrict__ free_slots, const float* __restrict__ new_mass,
+                                   const int32_t* __restrict__ new_plen, int B, long long next_request,
+                                   int slots, float* __restrict__ mass, int32_t* __restrict__ plen,
+                                   int64_t* __restrict__ request) {
+  const int i = blockIdx.x;
+  const long long s = free_slots[i];
+  if (s < 0 || s >= slots) return;
+  for (int b = threadIdx.x; b < B; b += blockDim.x) mass[s * B + b] = new_mass[(size_t)i * B + b];
+  if (threadIdx.x == 0) {
+    plen[s] = new_plen[i];
+    request[s] = next_request + i;
+  }
+}
+// Dispatch: the first `batch` slots of the order leave; their slots are
+// freed for the next arrivals and their request numbers reported.
+__global__ void queue_dispatch_kernel(const int32_t* __restrict__ order, int batch,
+                                      const int64_t* __restrict__ request, int slots,
+                                      int64_t* __restrict__ free_slots, int64_t* __restrict__ dispatched) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= batch) return;
+  const int s = order[i];
+  free_slots[i] = s;
+  dispatched[i] = (s >= 0 && s < slots) ? request[s] : -1;
+}
+
 }  // namespace
 
 hipError_t launch_ingest_panels(const float* src, int rows, int d, uint16_t* dst, hipStream_t stream) {
@@ -168,6 +197,25 @@ hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, 
   LaunchScope scope("store_insert", stream);
   hipLaunchKernelGGL(store_insert_kernel, dim3(grid_for(work, 256, 8192)), dim3(256), 0, stream, emb, out_len,
                      n, d, first, total, cap, ring_emb, ring_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_queue_admit(const int64_t* free_slots, int batch, const float* new_mass,
+                              const int32_t* new_plen, int B, long long next_request, int slots, float* mass,
+                              int32_t* plen, int64_t* request, hipStream_t stream) {
+  if (batch == 0) return hipSuccess;
+  LaunchScope scope("queue_admit", stream);
+  hipLaunchKernelGGL(queue_admit_kernel, dim3(batch), dim3(256), 0, stream, free_slots, new_mass, new_plen, B,
+                     next_request, slots, mass, plen, request);
+  return hipGetLastError();
+}
+
+hipError_t launch_queue_dispatch(const int32_t* order, int batch, const int64_t* request, int slots,
+                                 int64_t* free_slots, int64_t* dispatched, hipStream_t stream) {
+  if (batch == 0) return hipSuccess;
+  LaunchScope scope("queue_dispatch", stream);
+  hipLaunchKernelGGL(queue_dispatch_kernel, dim3((batch + 255) / 256), dim3(256), 0, stream, order, batch,
+                     request, slots, free_slots, dispatched);
   return hipGetLastError();
 }
 

@@ -266,6 +266,44 @@ SAGE_API int sage_store_insert(const float* emb, const int32_t* out_len, int n, 
                     "store_insert launch");
 }
 
+// ------------------------------------------------------------- queue
+SAGE_API int sage_queue_admit(const int64_t* free_slots, int batch, const float* new_mass,
+                              const int32_t* new_plen, int B, long long next_request, int slots, float* mass,
+                              int32_t* plen, int64_t* request, sage_stream_t stream) {
+  if (batch < 0) return fail(SAGE_EINVAL, "batch=%d is negative", batch);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (slots < batch) return fail(SAGE_EINVAL, "slots=%d is smaller than batch=%d", slots, batch);
+  if (next_request < 0) return fail(SAGE_EINVAL, "next_request=%lld is negative", next_request);
+  if (batch == 0) return ok();
+  const void* ptrs[] = {free_slots, new_mass, new_plen, mass, plen, request};
+  for (const void* p : ptrs) {
+    if (!p) return fail(SAGE_EINVAL, "sage_queue_admit: NULL pointer");
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_queue_admit: misaligned pointer");
+  }
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_queue_admit(free_slots, batch, new_mass, new_plen, B, next_request, slots, mass,
+                                             plen, request, (hipStream_t)stream),
+                    "queue_admit launch");
+}
+
+SAGE_API int sage_queue_dispatch(const int32_t* order, int batch, const int64_t* request, int slots,
+                                 int64_t* free_slots, int64_t* dispatched, sage_stream_t stream) {
+  if (batch < 0) return fail(SAGE_EINVAL, "batch=%d is negative", batch);
+  if (slots < batch) return fail(SAGE_EINVAL, "slots=%d is smaller than batch=%d", slots, batch);
+  if (batch == 0) return ok();
+  const void* ptrs[] = {order, request, free_slots, dispatched};
+  for (const void* p : ptrs) {
+    if (!p) return fail(SAGE_EINVAL, "sage_queue_dispatch: NULL pointer");
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_queue_dispatch: misaligned pointer");
+  }
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_queue_dispatch(order, batch, request, slots, free_slots, dispatched,
+                                                (hipStream_t)stream),
+                    "queue_dispatch launch");
+}
+
 // ------------------------------------------------------------- predict
 namespace {
 int check_predict_sizes(int Q, int N, int d, int k, int B) {

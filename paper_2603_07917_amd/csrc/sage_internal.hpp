@@ -79,6 +79,11 @@ hipError_t launch_ingest_panels(const float* src, int rows, int d, uint16_t* dst
 hipError_t launch_panels_from_rows(const uint16_t* src, int rows, int d, uint16_t* dst, hipStream_t stream);
 hipError_t launch_store_insert(const float* emb, const int32_t* out_len, int n, int d, long long total,
                                int cap, uint16_t* ring_emb, int32_t* ring_len, hipStream_t stream);
+hipError_t launch_queue_admit(const int64_t* free_slots, int batch, const float* new_mass,
+                              const int32_t* new_plen, int B, long long next_request, int slots, float* mass,
+                              int32_t* plen, int64_t* request, hipStream_t stream);
+hipError_t launch_queue_dispatch(const int32_t* order, int batch, const int64_t* request, int slots,
+                                 int64_t* free_slots, int64_t* dispatched, hipStream_t stream);
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
                        float* cost, hipStream_t stream);
 hipError_t launch_mix_uniform(const float* mass, int Q, int B, float weight, float* out,

@@ -48,6 +48,8 @@ def load_library():
         "sage_index_variant": (I, [P, P, P, I, I, I, I, F, P, P, S]),
         "sage_histogram_variant": (I, [P, P, I, I, P, I, F, P, I, I, P, P, S]),
         "sage_store_insert": (I, [P, P, I, I, ctypes.c_longlong, I, P, P, S]),
+        "sage_queue_admit": (I, [P, I, P, P, I, ctypes.c_longlong, I, P, P, P, S]),
+        "sage_queue_dispatch": (I, [P, I, P, I, P, P, S]),
         "sage_rank_workspace_bytes": (Z, [I]),
         "sage_rank": (I, [P, I, P, P, Z, S]),
         "sage_simulate": (I, [P, P, P, I, P, I, I, I, I, ctypes.c_double, I, P, P]),
@@ -448,8 +450,8 @@ class Queue:
     prompt length. A decision predicts the new arrivals into the slots freed by
     the previous dispatch, re-indexes every slot, ranks them and dispatches the
     first `batch` (smallest index first), whose slots take the next arrivals.
-    Buffers are allocated once; the per-decision bookkeeping (slot refills) is
-    plain tensor indexing.
+    Buffers are allocated once; the per-decision bookkeeping (slot refills and
+    the dispatched ids) runs in the library's queue kernels.
     """
 
     def __init__(self, store: Store, mass: torch.Tensor, prompt_len: torch.Tensor, batch: int):
@@ -477,8 +479,6 @@ class Queue:
                       torch.empty((self.batch, k), dtype=torch.float32, device=dev),
                       torch.empty((self.batch, B), dtype=torch.int32, device=dev),
                       torch.empty((self.batch, B), dtype=torch.float32, device=dev))
-        self._arange = torch.arange(self.batch, dtype=torch.int64, device=dev)
-        self._new_ids = torch.empty(self.batch, dtype=torch.int64, device=dev)
         self.dispatched = torch.empty(self.batch, dtype=torch.int64, device=dev)
 
     def decide(self, queries: torch.Tensor, prompt_len: torch.Tensor):
@@ -489,15 +489,19 @@ class Queue:
         if queries.shape[0] != self.batch or prompt_len.shape[0] != self.batch:
             raise SageError(f"a decision admits exactly {self.batch} requests")
         pred = self.store.predict(queries, out=self._pred)
-        self.mass.index_copy_(0, self.free, pred[3])
-        self.prompt_len.index_copy_(0, self.free, prompt_len)
-        torch.add(self._arange, self.next_request, out=self._new_ids)
-        self.request.index_copy_(0, self.free, self._new_ids)
+        if prompt_len.data_ptr() % 16 != 0 or not prompt_len.is_contiguous():
+            prompt_len = prompt_len.clone()
+        _dev(prompt_len, torch.int32, "prompt_len", 1)
+        lib = load_library()
+        B = self.mass.shape[1]
+        _check(lib.sage_queue_admit(_ptr(self.free), self.batch, _ptr(pred[3]), _ptr(prompt_len), B,
+                                    self.next_request, self.slots, _ptr(self.mass), _ptr(self.prompt_len),
+                                    _ptr(self.request), _stream()))
         self.next_request += self.batch
         index(self.mass, self.prompt_len, self.store.bin_repr, out=self.index)
         rank(self.index, workspace=self._rank_ws, out=self.order)
-        self.free.copy_(self.order[:self.batch])
-        torch.index_select(self.request, 0, self.free, out=self.dispatched)
+        _check(lib.sage_queue_dispatch(_ptr(self.order), self.batch, _ptr(self.request), self.slots,
+                                       _ptr(self.free), _ptr(self.dispatched), _stream()))
         return pred, self.dispatched
 
 

@@ -45,6 +45,8 @@ def lib():
     lib.sage_ingest_bf16_panels.argtypes = [P, I, I, P, P]
     lib.sage_panels_from_rows.argtypes = [P, I, I, P, P]
     lib.sage_predict_layout.argtypes = [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, P, Z, P]
+    lib.sage_queue_admit.argtypes = [P, I, P, P, I, ctypes.c_longlong, I, P, P, P, P]
+    lib.sage_queue_dispatch.argtypes = [P, I, P, I, P, P, P]
     lib.sage_status_string.restype = ctypes.c_char_p
     lib.sage_last_error.restype = ctypes.c_char_p
     return lib
@@ -120,6 +122,23 @@ def test_panels_ingest_validation(lib):
         assert fn(A, 10, 64, A + 16, None) == SAGE_EINVAL         # overlapping
         assert fn(A, 1 << 30, 64, A + 0x100000, None) == SAGE_EINVAL
         assert fn(None, 0, 64, None, None) == SAGE_OK              # nothing to do
+
+
+def test_queue_validation(lib):
+    adm, dis = lib.sage_queue_admit, lib.sage_queue_dispatch
+    a = [A + 0x1000 * i for i in range(6)]
+    assert adm(a[0], -1, a[1], a[2], 16, 0, 10, a[3], a[4], a[5], None) == SAGE_EINVAL
+    assert adm(a[0], 8, a[1], a[2], 0, 0, 10, a[3], a[4], a[5], None) == SAGE_EINVAL       # B
+    assert adm(a[0], 8, a[1], a[2], 16, 0, 7, a[3], a[4], a[5], None) == SAGE_EINVAL       # slots < batch
+    assert adm(a[0], 8, a[1], a[2], 16, -1, 10, a[3], a[4], a[5], None) == SAGE_EINVAL     # next_request
+    assert adm(None, 8, a[1], a[2], 16, 0, 10, a[3], a[4], a[5], None) == SAGE_EINVAL
+    assert adm(a[0] + 4, 8, a[1], a[2], 16, 0, 10, a[3], a[4], a[5], None) == SAGE_EINVAL
+    assert adm(None, 0, None, None, 16, 0, 0, None, None, None, None) == SAGE_OK           # nothing to do
+    assert dis(a[0], -1, a[1], 10, a[2], a[3], None) == SAGE_EINVAL
+    assert dis(a[0], 8, a[1], 7, a[2], a[3], None) == SAGE_EINVAL
+    assert dis(a[0], 8, None, 10, a[2], a[3], None) == SAGE_EINVAL
+    assert dis(a[0], 8, a[1], 10, a[2] + 8, a[3], None) == SAGE_EINVAL
+    assert dis(None, 0, None, 0, None, None, None) == SAGE_OK
 
 
 def test_predict_workspace_too_small(lib):

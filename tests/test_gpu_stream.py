@@ -75,3 +75,43 @@ def test_streaming_decisions_vs_oracle():
         assert np.array_equal(host(queue.free), order[:batch])
         print(f"call {call}: {int(clean.sum())}/{batch} rows compared through the index; "
               f"dispatched {want}", flush=True)
+
+
+@pytest.mark.parametrize("slots,batch,B", [(8200, 8, 512), (100, 100, 7), (5000, 37, 256)])
+def test_queue_admit_dispatch_match_indexing(slots, batch, B):
+    """The queue kernels against the same bookkeeping written as tensor indexing;
+    a slot outside [0, slots) is skipped by admit and reported as -1 by dispatch."""
+    lib = sage.load_library()
+    rng = np.random.default_rng(slots + batch)
+    mass = dev(rng.random((slots, B), dtype=np.float32))
+    plen = dev(rng.integers(1, 9000, slots).astype(np.int32))
+    request = dev(rng.integers(0, 10**6, slots).astype(np.int64))
+    free = rng.choice(slots, size=batch, replace=False).astype(np.int64)
+    if batch > 2:
+        free[1] = -1
+        free[2] = slots
+    new_mass = dev(rng.random((batch, B), dtype=np.float32))
+    new_plen = dev(rng.integers(1, 9000, batch).astype(np.int32))
+    want_mass, want_plen, want_req = host(mass).copy(), host(plen).copy(), host(request).copy()
+    for i, s in enumerate(free):
+        if 0 <= s < slots:
+            want_mass[s] = host(new_mass)[i]
+            want_plen[s] = host(new_plen)[i]
+            want_req[s] = 12345 + i
+    free_d = dev(free)
+    assert lib.sage_queue_admit(sage._ptr(free_d), batch, sage._ptr(new_mass), sage._ptr(new_plen), B, 12345,
+                                slots, sage._ptr(mass), sage._ptr(plen), sage._ptr(request), sage._stream()) == 0
+    assert np.array_equal(host(mass), want_mass)
+    assert np.array_equal(host(plen), want_plen)
+    assert np.array_equal(host(request), want_req)
+    order = rng.permutation(slots).astype(np.int32)
+    if batch > 1:
+        order[0] = slots + 3
+    out_free = torch.empty(batch, dtype=torch.int64, device="cuda")
+    out_disp = torch.empty(batch, dtype=torch.int64, device="cuda")
+    assert lib.sage_queue_dispatch(sage._ptr(dev(order)), batch, sage._ptr(request), slots, sage._ptr(out_free),
+                                   sage._ptr(out_disp), sage._stream()) == 0
+    assert np.array_equal(host(out_free), order[:batch].astype(np.int64))
+    req = host(request)
+    want = np.array([req[s] if 0 <= s < slots else -1 for s in order[:batch]], dtype=np.int64)
+    assert np.array_equal(host(out_disp), want)
