@@ -426,9 +426,6 @@ def run_ttlt(args, torch, sage, workloads):
                 torch.empty((n, B), dtype=torch.int32, device="cuda"))
     L = simulator.refresh_levels(tr.output_len, bucket)
     table = torch.empty((L, R), dtype=torch.float32, device="cuda")
-    gen = torch.empty((L, R), dtype=torch.int32, device="cuda")
-    for lv in range(L):
-        gen[lv].fill_(lv * bucket)
     g_static = torch.empty(R, dtype=torch.float32, device="cuda")
     g_mean = torch.empty(R, dtype=torch.float32, device="cuda")
     arr32 = dev(tr.arrival.astype(np.float32))
@@ -447,8 +444,7 @@ def run_ttlt(args, torch, sage, workloads):
         sage.rank(g_mean, workspace=rws, out=orders["mean"])
         sage.index(mass, plen, store.bin_repr, out=g_static)
         sage.rank(g_static, workspace=rws, out=orders["gittins-static"])
-        for lv in range(L):
-            sage.index_attained(mass, plen, store.bin_repr, gen[lv], bucket, out=table[lv])
+        sage.index_attained_table(mass, plen, store.bin_repr, L, bucket, out=table)
         sage.rank(table.view(-1), workspace=rws, out=orders["gittins"])
 
     log("warmup")

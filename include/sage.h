@@ -251,6 +251,20 @@ int sage_index_attained(const float* mass, const int32_t* prompt_len, const doub
                         float* index, int32_t* argmin_bin, sage_stream_t stream);
 
 /*
+ * sage_index_attained_table - sage_index_attained for every request at each
+ * refresh level at once: index[lv * Q + q] is request q's index after
+ * o = lv * bucket generated tokens (a = o^2 / 2 + I_q o), lv = 0 .. levels-1,
+ * the values sage_index_attained gives with generated[q] = lv * bucket. One
+ * read of each row serves all its levels (the table a trace replay orders
+ * by, Sec. 3.3: indices change only at bucket boundaries).
+ *   mass [Q, B] f32, prompt_len [Q] int32, bin_repr [B] f64, bucket >= 1,
+ *   levels >= 1 (levels * bucket within int32); index [levels, Q] f32 out.
+ * Errors as sage_index_attained; SAGE_EINVAL also for levels < 1.
+ */
+int sage_index_attained_table(const float* mass, const int32_t* prompt_len, const double* bin_repr,
+                              int bucket, int levels, int Q, int B, float* index, sage_stream_t stream);
+
+/*
  * Variants of the method that the paper compares against (Sec. 4 ablation).
  *
  * sage_histogram_variant - sage_histogram with a choice of neighbour weight:

@@ -61,17 +61,25 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     __syncthreads();
   }
 
-  float p[C], p_next[C];
+  float p[C], p_next[C], p_row[C];
+  // Refresh table (kAttained with var.levels > 0): every row at each level
+  // o = lv * bucket, from one read of the row; index[lv * Q + q].
+  const int n_lv = (kMode == kAttained && var.levels > 0) ? var.levels : 1;
   if (wave < Q) load_row<C, kFull>(mass, (size_t)wave * B, b0, B, p_next);
   for (int q = wave; q < Q; q += n_waves) {
     const size_t row = (size_t)q * (size_t)B;
 #pragma unroll
-    for (int j = 0; j < C; ++j) p[j] = p_next[j];
+    for (int j = 0; j < C; ++j) p_row[j] = p_next[j];
     if (q + n_waves < Q) load_row<C, kFull>(mass, row + (size_t)n_waves * B, b0, B, p_next);   // prefetch
     const double I = kFused ? (double)prompt_len[q] : 0.0;
+   for (int lv = 0; lv < n_lv; ++lv) {
+#pragma unroll
+    for (int j = 0; j < C; ++j) p[j] = p_row[j];
+    const size_t out = (size_t)lv * (size_t)Q + (size_t)q;
     double a = 0.0;                                 // service already received
     if (kMode == kAttained) {
-      const double o = (double)((max(generated[q], 0) / bucket) * bucket);
+      const double o = var.levels > 0 ? (double)lv * (double)bucket
+                                      : (double)((max(generated[q], 0) / bucket) * bucket);
       a = o * fma(0.5, o, I);
     }
 
@@ -124,8 +132,8 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     if (kMode == kVariant && var.kind == 1) {        // the mean: sum p x / sum p
       const double s_incl = s_base + lane_s;
       if (lane == kWave - 1) {
-        index[q] = f_total > 0.0 ? (float)(s_incl / f_total) : __builtin_inff();
-        if (kArg) argmin[q] = -1;
+        index[out] = f_total > 0.0 ? (float)(s_incl / f_total) : __builtin_inff();
+        if (kArg) argmin[out] = -1;
       }
       continue;
     }
@@ -181,9 +189,10 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     }
     if (lane == kWave - 1) {
       const bool found = r < __builtin_inf();
-      index[q] = found ? (float)r : __builtin_inff();
-      if (kArg) argmin[q] = found ? best_b : -1;
+      index[out] = found ? (float)r : __builtin_inff();
+      if (kArg) argmin[out] = found ? best_b : -1;
     }
+   }
   }
 }
 
@@ -214,7 +223,8 @@ hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* p
                           const double* repr, const int32_t* generated, int bucket, int Q, int B,
                           float* index, int32_t* argmin, hipStream_t stream, const IndexVariant* variant) {
   const bool full = B == 64 * C;
-  const int mode = variant ? kVariant : (generated ? kAttained : (cost ? kGivenCost : kFused));
+  const int mode = (variant && variant->levels > 0) ? kAttained
+                   : variant ? kVariant : (generated ? kAttained : (cost ? kGivenCost : kFused));
   const IndexVariant var = variant ? *variant : IndexVariant();
 #define SAGE_INDEX_LAUNCH(FULL, MODE)                                                               \
   return launch_index_v<C, FULL, MODE>(mass, cost, prompt_len, repr, generated, bucket, Q, B, index, \
@@ -469,7 +479,9 @@ hipError_t launch_index(const float* mass, const float* cost, const int32_t* pro
                         const double* bin_repr, const int32_t* generated, int bucket, int Q, int B,
                         float* index, int32_t* argmin, hipStream_t stream, const IndexVariant* variant) {
   if (Q == 0) return hipSuccess;
-  LaunchScope scope(variant ? "index_variant" : (generated ? "index_attained" : "index_scan"), stream);
+  LaunchScope scope(variant ? (variant->levels > 0 ? "index_attained_table" : "index_variant")
+                            : (generated ? "index_attained" : "index_scan"),
+                    stream);
   const int per_lane = (B + kWave - 1) / kWave;
 #define SAGE_INDEX_C(CC) \
   return launch_index_c<CC>(mass, cost, prompt_len, bin_repr, generated, bucket, Q, B, index, argmin, stream, \

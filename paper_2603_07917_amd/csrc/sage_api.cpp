@@ -507,6 +507,29 @@ SAGE_API int sage_index_attained(const float* mass, const int32_t* prompt_len, c
                     "index launch");
 }
 
+SAGE_API int sage_index_attained_table(const float* mass, const int32_t* prompt_len, const double* bin_repr,
+                                       int bucket, int levels, int Q, int B, float* index, sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (bucket < 1) return fail(SAGE_EINVAL, "bucket=%d must be >= 1", bucket);
+  if (levels < 1) return fail(SAGE_EINVAL, "levels=%d must be >= 1", levels);
+  if ((double)levels * (double)bucket > 2147483647.0)
+    return fail(SAGE_EINVAL, "levels * bucket = %.0f exceeds the int32 token range", (double)levels * bucket);
+  if (Q == 0) return ok();
+  if (!mass || !prompt_len || !bin_repr || !index)
+    return fail(SAGE_EINVAL, "sage_index_attained_table: NULL required pointer");
+  const void* ptrs[] = {mass, prompt_len, bin_repr, index};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_index_attained_table: misaligned pointer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  sage::IndexVariant table;
+  table.levels = levels;
+  return hip_status(sage::launch_index(mass, nullptr, prompt_len, bin_repr, nullptr, bucket, Q, B, index, nullptr,
+                                       (hipStream_t)stream, &table),
+                    "index table launch");
+}
+
 // ----------------------------------------------------------------- rank
 SAGE_API size_t sage_rank_workspace_bytes(int Q) { return Q > 0 ? sage::rank_workspace_bytes(Q) : 0; }
 

@@ -94,6 +94,7 @@ struct IndexVariant {
   int cost_model = 0;
   int kind = 0;
   float noise = 0.0f;
+  int levels = 0;     // > 0: the refreshed index at o = 0, bucket, ..., (levels - 1) * bucket
 };
 hipError_t launch_index(const float* mass, const float* cost, const int32_t* prompt_len,
                         const double* bin_repr, const int32_t* generated, int bucket, int Q, int B,

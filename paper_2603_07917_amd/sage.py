@@ -45,6 +45,7 @@ def load_library():
         "sage_cost": (I, [P, I, P, I, P, S]),
         "sage_index": (I, [P, P, P, P, I, I, P, P, S]),
         "sage_index_attained": (I, [P, P, P, P, I, I, I, P, P, S]),
+        "sage_index_attained_table": (I, [P, P, P, I, I, I, I, P, S]),
         "sage_index_variant": (I, [P, P, P, I, I, I, I, F, P, P, S]),
         "sage_histogram_variant": (I, [P, P, I, I, P, I, F, P, I, I, P, P, S]),
         "sage_store_insert": (I, [P, P, I, I, ctypes.c_longlong, I, P, P, S]),
@@ -238,6 +239,23 @@ def index_attained(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch
                                               _ptr(generated), int(bucket), Q, B, _ptr(g), _ptr(arg),
                                               _stream()))
     return (g, arg) if with_argmin else g
+
+
+def index_attained_table(mass: torch.Tensor, prompt_len: torch.Tensor, bin_repr: torch.Tensor, levels: int,
+                         bucket: int = 200, out: Optional[torch.Tensor] = None):
+    """Refresh table: [levels, Q] indices, row lv after lv * bucket generated tokens."""
+    _dev(mass, torch.float32, "mass", 2)
+    _dev(prompt_len, torch.int32, "prompt_len", 1)
+    _dev(bin_repr, torch.float64, "bin_repr", 1)
+    Q, B = mass.shape
+    if prompt_len.shape[0] != Q or bin_repr.shape[0] != B:
+        raise SageError("prompt_len / bin_repr do not match mass")
+    g = out if out is not None else torch.empty((levels, Q), dtype=torch.float32, device=mass.device)
+    if tuple(g.shape) != (levels, Q) or not g.is_contiguous():
+        raise SageError("out must be a contiguous [levels, Q] tensor")
+    _check(load_library().sage_index_attained_table(_ptr(mass), _ptr(prompt_len), _ptr(bin_repr), int(bucket),
+                                                    int(levels), Q, B, _ptr(g), _stream()))
+    return g
 
 
 COST_MODELS = {"resource": 0, "output": 1, "overall": 2}

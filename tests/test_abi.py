@@ -45,6 +45,7 @@ def lib():
     lib.sage_ingest_bf16_panels.argtypes = [P, I, I, P, P]
     lib.sage_panels_from_rows.argtypes = [P, I, I, P, P]
     lib.sage_predict_layout.argtypes = [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, P, Z, P]
+    lib.sage_index_attained_table.argtypes = [P, P, P, I, I, I, I, P, P]
     lib.sage_queue_admit.argtypes = [P, I, P, P, I, ctypes.c_longlong, I, P, P, P, P]
     lib.sage_queue_dispatch.argtypes = [P, I, P, I, P, P, P]
     lib.sage_status_string.restype = ctypes.c_char_p
@@ -122,6 +123,19 @@ def test_panels_ingest_validation(lib):
         assert fn(A, 10, 64, A + 16, None) == SAGE_EINVAL         # overlapping
         assert fn(A, 1 << 30, 64, A + 0x100000, None) == SAGE_EINVAL
         assert fn(None, 0, 64, None, None) == SAGE_OK              # nothing to do
+
+
+def test_index_table_validation(lib):
+    fn = lib.sage_index_attained_table
+    a = [A + 0x1000 * i for i in range(4)]
+    assert fn(a[0], a[1], a[2], 200, 5, -1, 16, a[3], None) == SAGE_EINVAL      # Q
+    assert fn(a[0], a[1], a[2], 200, 5, 10, 0, a[3], None) == SAGE_EINVAL       # B
+    assert fn(a[0], a[1], a[2], 0, 5, 10, 16, a[3], None) == SAGE_EINVAL        # bucket
+    assert fn(a[0], a[1], a[2], 200, 0, 10, 16, a[3], None) == SAGE_EINVAL      # levels
+    assert fn(a[0], a[1], a[2], 1 << 20, 1 << 12, 10, 16, a[3], None) == SAGE_EINVAL   # token range
+    assert fn(None, a[1], a[2], 200, 5, 10, 16, a[3], None) == SAGE_EINVAL
+    assert fn(a[0], a[1] + 4, a[2], 200, 5, 10, 16, a[3], None) == SAGE_EINVAL
+    assert fn(None, None, None, 200, 5, 0, 16, None, None) == SAGE_OK           # nothing to do
 
 
 def test_queue_validation(lib):

@@ -160,6 +160,31 @@ def test_index_attained_vs_oracle_full_index_workload():
     print(f"attained: {int((gen > 0).sum())} running rows, {int(inf.sum())} with no mass left")
 
 
+@pytest.mark.parametrize("B,levels,bucket", [(256, 41, 200), (100, 5, 1), (1024, 3, 500), (7, 1, 200)])
+def test_index_attained_table_matches_per_level_calls(B, levels, bucket):
+    """The refresh table equals sage_index_attained called level by level (same
+    arithmetic, bit for bit), and level 0 equals the arrival index."""
+    rng = np.random.default_rng(B + levels)
+    Q = 777
+    mass = rng.dirichlet(np.full(B, 0.3), size=Q).astype(np.float32)
+    mass[:3] = 0.0                                                # empty rows: +inf everywhere
+    plen = rng.integers(8, 4000, size=Q).astype(np.int32)
+    edges, r = workloads.log_bins(16384, B)
+    md, pd, rd = dev(mass), dev(plen), dev(r)
+    table = host(sage.index_attained_table(md, pd, rd, levels, bucket))
+    for lv in range(levels):
+        g = host(sage.index_attained(md, pd, rd, dev(np.full(Q, lv * bucket, np.int32)), bucket))
+        assert np.array_equal(table[lv].view(np.uint32), g.view(np.uint32)), lv
+    assert np.array_equal(table[0].view(np.uint32), host(sage.index(md, pd, rd)).view(np.uint32))
+    x = oracle.cost(plen, r)
+    G, _ = oracle.gittins_attained(mass.astype(np.float64), x,
+                                   oracle.attained_service(plen, np.full(Q, (levels - 1) * bucket), bucket))
+    inf = np.isinf(G)
+    assert np.array_equal(np.isinf(table[-1]), inf)
+    rel = np.abs(table[-1][~inf].astype(np.float64) - G[~inf]) / G[~inf]
+    assert rel.max(initial=0.0) <= parity.INDEX_RTOL
+
+
 @pytest.mark.parametrize("B", [7, 64, 256, 1024])
 def test_index_attained_zero_is_the_index_and_argmin(B):
     rng = np.random.default_rng(B)
