@@ -66,6 +66,10 @@ CASES = [
     (16, 20000, 64, 1, 16),
     (9, 65536, 32, 64, 32),
     (4, 40000, 2080, 32, 64),   # d above the stream path's limit: the list path
+    (17, 30000, 64, 100, 64),   # one query past the stream path: the list path
+    (17, 30000, 64, 64, 64),    # ... and the filtered path
+    (4, 16384, 64, 128, 32),    # the smallest store with a threshold sample at k = 128: stream path
+    (4, 16383, 64, 128, 32),    # one row less: no sample, the list path without a threshold
 ]
 
 
