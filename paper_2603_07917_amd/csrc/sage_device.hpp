@@ -40,17 +40,10 @@ __device__ __forceinline__ float key_sim(uint64_t k) { return f32_from_order_bit
 __device__ __forceinline__ int32_t key_id(uint64_t k) { return (int32_t)(~(uint32_t)k); }
 
 // ---------------------------------------------------------------------------
-// Cross-lane moves within a 64-wide wavefront: ds_bpermute for a lane chosen
-// at run time, DPP and the lane-swap instructions for fixed strides.
+// Cross-lane moves within a 64-wide wavefront: DPP and the lane-swap
+// instructions for fixed strides, readlane for a fixed lane.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
-
-__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src_lane) {
-  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-  lo = (uint32_t)__shfl((int)lo, src_lane, kWave);
-  hi = (uint32_t)__shfl((int)hi, src_lane, kWave);
-  return ((uint64_t)hi << 32) | lo;
-}
 
 // Value held by lane (lane ^ S), for a stride S fixed at compile time, with
 // no LDS round trip: DPP within a row of 16 lanes (S = 1, 2: quad
@@ -124,7 +117,6 @@ __device__ __forceinline__ uint64_t wave_sort64(uint64_t v, bool descending) {
   }
   return v;
 }
-__device__ __forceinline__ uint64_t wave_sort_desc64(uint64_t v) { return wave_sort64(v, true); }
 
 // ---------------------------------------------------------------------------
 // Wave reductions / scans.
