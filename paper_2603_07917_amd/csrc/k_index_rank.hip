@@ -315,7 +315,7 @@ __global__ void __launch_bounds__(256) rank_scan_kernel(uint32_t* __restrict__ h
 __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
     const float* __restrict__ g_in, const uint32_t* __restrict__ k_in,
     const uint32_t* __restrict__ v_in, int Q, int shift, int n_tiles,
-    const uint32_t* __restrict__ offsets, const uint32_t* __restrict__ digit_total,
+    const uint32_t* __restrict__ offsets, const uint32_t* __restrict__ digit_total, int fused,
     uint32_t* __restrict__ k_out, uint32_t* __restrict__ v_out) {
   constexpr int kWaves = kRankThreads / kWave;
   __shared__ uint32_t base_off[256];
@@ -326,8 +326,22 @@ __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
   const int w = t / kWave;
   {
     // exclusive scan of the 256 digit totals (one per thread), plus this
-    // tile's offset within the digit
-    const uint32_t v = digit_total[t];
+    // tile's offset within the digit. `fused` (few tiles): both from the raw
+    // per-tile counts, offsets[digit][tile], read here (no scan kernel).
+    uint32_t v, tile_off;
+    if (fused) {
+      const uint32_t* row = offsets + (size_t)t * n_tiles;
+      v = 0;
+      tile_off = 0;
+      for (int i = 0; i < n_tiles; ++i) {
+        const uint32_t c = row[i];
+        if (i == (int)blockIdx.x) tile_off = v;
+        v += c;
+      }
+    } else {
+      v = digit_total[t];
+      tile_off = offsets[t * n_tiles + blockIdx.x];
+    }
     uint32_t incl = v;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
@@ -338,7 +352,7 @@ __global__ void __launch_bounds__(kRankThreads) rank_scatter_kernel(
     __syncthreads();
     uint32_t before = 0;
     for (int ww = 0; ww < w; ++ww) before += running[ww];
-    base_off[t] = before + incl - v + offsets[t * n_tiles + blockIdx.x];
+    base_off[t] = before + incl - v + tile_off;
     __syncthreads();
   }
   running[t] = 0;
@@ -517,6 +531,9 @@ hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipS
   uint32_t* vB = kB + Q;
   uint32_t* hist = vB + Q;
   uint32_t* totals = hist + 256 * (size_t)n_tiles;
+  // With few tiles each scatter workgroup sums the per-tile counts itself
+  // (n_tiles loads per digit) and the scan launch is skipped.
+  const bool fused = n_tiles <= 64;
   const uint32_t* k_in = nullptr;
   const uint32_t* v_in = nullptr;
   for (int pass = 0; pass < 4; ++pass) {
@@ -529,14 +546,14 @@ hipError_t launch_rank(const float* index, int Q, int32_t* order, void* ws, hipS
       hipLaunchKernelGGL(rank_hist_kernel, dim3(n_tiles), dim3(kRankThreads), 0, stream, index, k_in,
                          Q, shift, n_tiles, hist);
     }
-    {
+    if (!fused) {
       LaunchScope scope("rank_scan", stream);
       hipLaunchKernelGGL(rank_scan_kernel, dim3(256), dim3(256), 0, stream, hist, n_tiles, totals);
     }
     {
       LaunchScope scope("rank_scatter", stream);
       hipLaunchKernelGGL(rank_scatter_kernel, dim3(n_tiles), dim3(kRankThreads), 0, stream, index,
-                         k_in, v_in, Q, shift, n_tiles, hist, totals, k_out, v_out);
+                         k_in, v_in, Q, shift, n_tiles, hist, totals, fused ? 1 : 0, k_out, v_out);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
