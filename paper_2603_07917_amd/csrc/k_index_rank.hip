@@ -36,7 +36,8 @@ __device__ __forceinline__ void load_row(const float* __restrict__ mass, size_t 
 // x <= a are ruled out and the rest are shifted down by a, so the result is
 // the index of the remaining cost. kVariant takes the cost model, the kind
 // of index (Gittins or mean) and a uniform-mixing weight at run time.
-enum IndexMode { kGivenCost = 0, kFused = 1, kAttained = 2, kVariant = 3 };
+// kTable: kAttained for every row at each level o = lv * bucket (lv < levels).
+enum IndexMode { kGivenCost = 0, kFused = 1, kAttained = 2, kVariant = 3, kTable = 4 };
 // Workgroups per CU the register budget is tuned for (4 waves each).
 template <int C> struct IndexOcc { static constexpr int value = C <= 8 ? 4 : (C == 16 ? 3 : 1); };
 
@@ -61,25 +62,24 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     __syncthreads();
   }
 
-  float p[C], p_next[C], p_row[C];
-  // Refresh table (kAttained with var.levels > 0): every row at each level
-  // o = lv * bucket, from one read of the row; index[lv * Q + q].
-  const int n_lv = (kMode == kAttained && var.levels > 0) ? var.levels : 1;
+  float p[C], p_next[C];
+  // Refresh table (kTable): every row at each level o = lv * bucket, from
+  // one read of the row; index[lv * Q + q]. One level in every other mode.
+  constexpr bool kAtt = kMode == kAttained || kMode == kTable;
+  const int n_lv = kMode == kTable ? var.levels : 1;
   if (wave < Q) load_row<C, kFull>(mass, (size_t)wave * B, b0, B, p_next);
   for (int q = wave; q < Q; q += n_waves) {
     const size_t row = (size_t)q * (size_t)B;
 #pragma unroll
-    for (int j = 0; j < C; ++j) p_row[j] = p_next[j];
+    for (int j = 0; j < C; ++j) p[j] = p_next[j];
     if (q + n_waves < Q) load_row<C, kFull>(mass, row + (size_t)n_waves * B, b0, B, p_next);   // prefetch
     const double I = kFused ? (double)prompt_len[q] : 0.0;
    for (int lv = 0; lv < n_lv; ++lv) {
-#pragma unroll
-    for (int j = 0; j < C; ++j) p[j] = p_row[j];
     const size_t out = (size_t)lv * (size_t)Q + (size_t)q;
     double a = 0.0;                                 // service already received
-    if (kMode == kAttained) {
-      const double o = var.levels > 0 ? (double)lv * (double)bucket
-                                      : (double)((max(generated[q], 0) / bucket) * bucket);
+    if (kAtt) {
+      const double o = kMode == kTable ? (double)lv * (double)bucket
+                                       : (double)((max(generated[q], 0) / bucket) * bucket);
       a = o * fma(0.5, o, I);
     }
 
@@ -112,15 +112,17 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
           if (kFull || b0 + j < B) p[j] = (float)fma(keep, (double)p[j], spread);
       }
     }
-    if (kMode == kAttained) {                       // rule out the outcomes already passed
-#pragma unroll
-      for (int j = 0; j < C; ++j) p[j] = support(j) > a ? p[j] : 0.0f;
-    }
+    // The mass of bin j; with attained service, the outcomes already passed
+    // (x <= a) are ruled out (p itself is kept for the next level).
+    auto pm = [&](int j) -> double {
+      if (kAtt && !(support(j) > a)) return 0.0;
+      return (double)p[j];
+    };
     double lane_f = 0.0, lane_s = 0.0;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
-      lane_f += (double)p[j];
-      lane_s = fma((double)p[j], support(j) - a, lane_s);
+      lane_f += pm(j);
+      lane_s = fma(pm(j), support(j) - a, lane_s);
     }
     // Prefix sums over lanes (DPP); the mass above this lane is the row total
     // minus the inclusive prefix (fp64, so its rounding is ~1e-16 of the total).
@@ -147,7 +149,7 @@ __global__ void __launch_bounds__(256, IndexOcc<C>::value) index_kernel(const fl
     double f_run = f_base, s_run = s_base, t_run = f_total - f_base;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
-      const double pj = (double)p[j];
+      const double pj = pm(j);
       const double xj = support(j) - a;
       f_run += pj;
       s_run = fma(pj, xj, s_run);
@@ -223,7 +225,7 @@ hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* p
                           const double* repr, const int32_t* generated, int bucket, int Q, int B,
                           float* index, int32_t* argmin, hipStream_t stream, const IndexVariant* variant) {
   const bool full = B == 64 * C;
-  const int mode = (variant && variant->levels > 0) ? kAttained
+  const int mode = (variant && variant->levels > 0) ? kTable
                    : variant ? kVariant : (generated ? kAttained : (cost ? kGivenCost : kFused));
   const IndexVariant var = variant ? *variant : IndexVariant();
 #define SAGE_INDEX_LAUNCH(FULL, MODE)                                                               \
@@ -232,6 +234,10 @@ hipError_t launch_index_c(const float* mass, const float* cost, const int32_t* p
   if (mode == kVariant) {
     if (full) SAGE_INDEX_LAUNCH(true, kVariant);
     SAGE_INDEX_LAUNCH(false, kVariant);
+  }
+  if (mode == kTable) {
+    if (full) SAGE_INDEX_LAUNCH(true, kTable);
+    SAGE_INDEX_LAUNCH(false, kTable);
   }
   if (full) {
     if (mode == kAttained) SAGE_INDEX_LAUNCH(true, kAttained);
