@@ -41,22 +41,22 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // Device check, cached per device ordinal: the kernels are built for gfx950.
 int check_device() {
   static std::mutex mu;
-  static std::vector<int> verdict;   // 0 unknown, 1 ok, -1 unsupported
+  static std::vector<int> arch_state;   // 0 unknown, 1 ok, -1 unsupported
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SAGE_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
   std::lock_guard<std::mutex> lock(mu);
-  if ((int)verdict.size() <= dev) verdict.resize(dev + 1, 0);
-  if (verdict[dev] == 0) {
+  if ((int)arch_state.size() <= dev) arch_state.resize(dev + 1, 0);
+  if (arch_state[dev] == 0) {
     hipDeviceProp_t prop;
     e = hipGetDeviceProperties(&prop, dev);
     if (e != hipSuccess) return fail(SAGE_EHIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
-    verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
-    if (verdict[dev] < 0)
+    arch_state[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    if (arch_state[dev] < 0)
       return fail(SAGE_EUNSUPPORTED, "device %d is %s, the library is built for gfx950", dev,
                   prop.gcnArchName);
   }
-  if (verdict[dev] < 0) return fail(SAGE_EUNSUPPORTED, "device %d is not gfx950", dev);
+  if (arch_state[dev] < 0) return fail(SAGE_EUNSUPPORTED, "device %d is not gfx950", dev);
   return SAGE_OK;
 }
 
