@@ -12,9 +12,11 @@
 // to the query's candidate array with one global atomic per query. The
 // select kernel then folds each query's candidates into its top k.
 //
-// Every true neighbour scores >= theta0, so it is a candidate; a query whose
-// candidates overflow (a workgroup's LDS slots or the array) is flagged and
-// answered by the exact list path instead.
+// Every true neighbour scores >= theta0, so it is a candidate. A workgroup
+// whose LDS slots for a query fill up (a store with similar rows side by
+// side) sends the rest to the array one atomic at a time; a query whose
+// candidates overflow the array is flagged and answered by the exact list
+// path instead.
 #include "sage_device.hpp"
 #include "sage_internal.hpp"
 
@@ -91,7 +93,13 @@ __global__ void __launch_bounds__(kThreads) sim_stream_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if ((bits >> i) & 1u) {
-        if (pos < kLCap) lbuf[ql][pos] = make_key(acc[i], (uint32_t)(r0 + i));
+        const uint64_t key = make_key(acc[i], (uint32_t)(r0 + i));
+        if (pos < kLCap) {
+          lbuf[ql][pos] = key;
+        } else {                                   // slots full (clustered store): straight to the array
+          const int gpos = atomicAdd(&cand_count[ql], 1);
+          if (gpos < cap) cand[(size_t)ql * cap + gpos] = key;
+        }
         ++pos;
       }
     }
@@ -145,19 +153,18 @@ __global__ void __launch_bounds__(kThreads) sim_stream_kernel(
     }
   }
 
-  // Append this workgroup's candidates: one global atomic per query. A
-  // query past its LDS slots gets a count beyond the array instead, which
-  // flags it for the exact path.
+  // Append this workgroup's candidates: one global atomic per query for its
+  // LDS slots (keys past them went to the array one by one). A query whose
+  // count passes the array's capacity is flagged for the exact path.
   __syncthreads();
   if (tid < Q) {
-    const int n = lcnt[tid];
-    gbase[tid] = n == 0 ? 0 : atomicAdd(&cand_count[tid], n > kLCap ? cap + 1 : n);
+    const int n = min(lcnt[tid], kLCap);
+    gbase[tid] = n == 0 ? 0 : atomicAdd(&cand_count[tid], n);
   }
   __syncthreads();
   for (int i = tid; i < Q * kLCap; i += kThreads) {
     const int q = i / kLCap, e = i % kLCap;
-    const int n = lcnt[q];
-    if (n <= kLCap && e < n && gbase[q] + e < cap) cand[(size_t)q * cap + gbase[q] + e] = lbuf[q][e];
+    if (e < min(lcnt[q], kLCap) && gbase[q] + e < cap) cand[(size_t)q * cap + gbase[q] + e] = lbuf[q][e];
   }
 }
 

@@ -226,3 +226,21 @@ def test_config3_full_size_sampled():
     rows = np.unique(rows)
     clean = check_decision(w, rows, ids, sims, counts, mass, g, order, spec.k, spec.tau)
     print(f"config 3: {clean}/{len(rows)} sampled queries compared through the index", flush=True)
+
+
+def test_stream_path_clustered_store():
+    """Few queries against a store whose close neighbours sit side by side (a
+    FIFO window that received a burst of similar prompts): a workgroup sees
+    more candidates of a query than its LDS slots hold, and the rest go to the
+    query's candidate array one by one."""
+    Q, N, d, k = 4, 60000, 64, 64
+    w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=64, seed=77, clusters=6)
+    rng = np.random.default_rng(77)
+    for q in range(Q):
+        rows = slice(20000 + 1500 * q, 20000 + 1500 * (q + 1))
+        near = w.queries[q] + 0.02 * rng.standard_normal((1500, d)).astype(np.float32)
+        w.hist_emb[rows] = near / np.linalg.norm(near, axis=1, keepdims=True)
+    ids, sims, counts, mass = run_predict(w, k)
+    S = oracle_scores(w)
+    parity.check_predict(ids, sims, counts, mass, S, w.hist_len, w.bin_edges, 0.8, k)
+    assert np.all((ids >= 20000) & (ids < 26000))          # the burst holds every query's neighbours
