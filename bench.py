@@ -390,7 +390,8 @@ def run_streaming(args, torch, sage, workloads):
         "reindexed_rows_per_s": queue.slots * args.steps / elapsed,
         "roofline": {"bound": "hbm", "kernel": kernel_name(spec.k, batch), "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "avg_launch_us": k1_avg_s * 1e6, "bytes_per_launch": k1_bytes},
+                     "traffic": read_traffic("sim_stream_kernel", "streaming",
+                                             sources=("k_sim_stream.hip", "sage_device.hpp")), "avg_launch_us": k1_avg_s * 1e6, "bytes_per_launch": k1_bytes},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
     }
     print(json.dumps(line), flush=True)
