@@ -1078,10 +1078,14 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   // Threshold pre-pass: every SR-th step, >= 4k group maxima, at most 8192.
   // SR <= 16 on the filtered path (every candidate above theta0 is written
   // out there, so a tighter bound pays for the larger sample), else <= 32.
+  // The sample costs about Q N d / SR and the candidates about Q k SR, so the
+  // best SR grows with the square root of N d: from N d = 2^29 on (1M keys
+  // of d = 1024) the filtered path also samples every 32nd step.
   // Only whole steps are sampled.
   const long steps = (long)N / kStepRows;
   if (steps * 16 >= 8L * k) {
-    const long sr_max = L == 64 ? 16 : 32;
+    const bool wide = Q > kStreamMaxQ && (long)N * d >= (1L << 29);
+    const long sr_max = L == 64 && !wide ? 16 : 32;
     long sr = steps * 16 / (4L * k);
     if (sr > sr_max) sr = sr_max;
     if (sr < 1) sr = 1;
