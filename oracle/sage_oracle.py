@@ -81,9 +81,12 @@ def similarity(q_bits, h_bits) -> np.ndarray:
 
     Products of two bf16 values are exact in fp64; the sums are exact or
     within a few fp64 ulps for the dimensions used here. No renormalisation
-    after the bf16 rounding.
+    after the bf16 rounding. Either operand may be given as bf16 bit
+    patterns (uint16) or as their exact fp64 values (``bf16_to_f64``), so
+    that a large store is widened once for several query blocks.
     """
-    return bf16_to_f64(q_bits) @ bf16_to_f64(h_bits).T
+    widen = lambda a: a if np.asarray(a).dtype == np.float64 else bf16_to_f64(a)
+    return widen(q_bits) @ widen(h_bits).T
 
 
 # ------------------------------------------------------------------ top-k

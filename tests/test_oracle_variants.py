@@ -1,5 +1,6 @@
 """Pins of the oracle's variants of the method (the paper's ablations, Sec. 4):
 cost models, the Mean index, uniform-noise mixing, unweighted histogram."""
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -81,3 +82,56 @@ def test_unweighted_histogram_matches_exact(seed):
     assert np.allclose(m2, c2 / valid, rtol=0, atol=1e-15)
     with pytest.raises(ValueError):
         oracle.histogram(ids, sims, lengths, edges, 0.8, weighting="rank")
+
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_cost_models_golden():
+    """The three cost models against hand-derived values (golden/cost_models.txt)."""
+    n = 0
+    for line in open(os.path.join(GOLDEN, "cost_models.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        I, O, res, out, overall, _ = [f.strip() for f in line.split("|")]
+        I, O = np.array([int(I)]), np.array([float(O)])
+        for model, want in (("resource", res), ("output", out), ("overall", overall)):
+            assert oracle.cost_variant(I, O, model)[0, 0] == float(Fraction(want)), (model, I, O)
+        n += 1
+    assert n == 5
+
+
+def _policy_golden():
+    kv = {}
+    for line in open(os.path.join(GOLDEN, "policy_orders.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        key, val = line.split(":", 1)
+        kv[key.strip()] = val.strip()
+    return kv
+
+
+def test_policy_orders_golden():
+    """Each policy's queue order (FCFS, Mean, Gittins at arrival, Gittins
+    refreshed) and the index values behind it, against hand-derived values
+    (golden/policy_orders.txt)."""
+    from oracle import sage_sim
+    kv = _policy_golden()
+    frac = lambda s: [Fraction(v) for v in s.split()]
+    mass = np.array([[float(v) for v in frac(row)] for row in kv["masses"].split(";")])
+    repr_ = np.array([float(v) for v in frac(kv["repr"])])
+    plen = np.array([int(v) for v in kv["prompt_len"].split()], dtype=np.int32)
+    arrival = np.array([float(v) for v in kv["arrival"].split()])
+    out_len = np.array([int(v) for v in kv["output_len"].split()], dtype=np.int32)
+    x = oracle.cost(plen, repr_)
+    G, _ = oracle.gittins(mass, x)
+    assert np.allclose(G, [float(v) for v in frac(kv["gittins"])], rtol=1e-15, atol=0)
+    assert np.allclose(oracle.mean_index(mass, x), [float(v) for v in frac(kv["mean"])], rtol=1e-15, atol=0)
+    a1 = oracle.attained_service(plen, np.ones(4), 1)
+    g1, _ = oracle.gittins_attained(mass, x, a1)
+    assert np.allclose(g1, [float(v) for v in frac(kv["refreshed_level1"])], rtol=1e-15, atol=0)
+    for policy in ("fcfs", "mean", "gittins-static", "gittins"):
+        order, levels, informed = sage_sim.policy_order(policy, arrival, mass, plen, repr_, out_len, bucket=1)
+        want = [int(v) for v in kv[f"order {policy}"].split()]
+        assert list(order) == want, policy
+        assert levels == (2 if policy == "gittins" else 1) and informed == len(want)
