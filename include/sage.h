@@ -148,7 +148,10 @@ size_t sage_predict_workspace_bytes(int Q, int N, int d, int k, int B);
  *                         below it get zero weight (paper default 0.8)
  *   bin_edges [B+1] f64   strictly increasing length-bin edges; a length L
  *                         falls in the largest b in [0, B-1] with
- *                         edges[b] <= L (lengths below edges[0] go to bin 0)
+ *                         edges[b] <= L (lengths below edges[0] go to bin 0).
+ *                         The order is a precondition that is not checked
+ *                         before enqueue (device array): see
+ *                         sage_check_inputs
  *   B                     1..SAGE_MAX_BINS
  * Outputs (row q = request q):
  *   nbr_ids  [Q, k] int32 the k history indices with the largest similarity
@@ -205,6 +208,8 @@ int sage_histogram(const int32_t* nbr_ids, const float* nbr_sims, int Q, int k,
  * evaluated in fp64 and rounded to fp32.
  *   prompt_len [Q] int32 (>= 0), bin_repr [B] f64 representative output
  *   length of each bin (positive, increasing), cost [Q, B] f32 out.
+ *   Both orders are preconditions checked on the device by
+ *   sage_check_inputs, not before enqueue.
  */
 int sage_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
               float* cost, sage_stream_t stream);
@@ -314,6 +319,42 @@ enum { SAGE_INDEX_GITTINS = 0, SAGE_INDEX_MEAN = 1 };
 int sage_index_variant(const float* mass, const int32_t* prompt_len, const double* bin_repr, int Q, int B,
                        int cost_model, int index_kind, float noise_weight,
                        float* index, int32_t* argmin_bin, sage_stream_t stream);
+
+/*
+ * sage_check_inputs - device check of the preconditions that the binning and
+ * the index scan rely on but that validation before enqueue cannot see (the
+ * arrays are device-resident, and reading them on the host would synchronise
+ * the stream):
+ *   SAGE_CHECK_EDGES       bin_edges [B+1] finite and strictly increasing
+ *                          (the bins of Sec. 3.1's length histogram)
+ *   SAGE_CHECK_REPR        bin_repr [B] finite, bin_repr[0] >= 0, and
+ *                          non-decreasing
+ *   SAGE_CHECK_PROMPT_LEN  prompt_len [Q] >= 0
+ * With the last two the cost support r (I + r/2) of Sec. 3.2 is
+ * non-decreasing along every row, which the Gittins scan of Sec. 3.3 needs:
+ * on unsorted support sage_index returns a value that is not the index, and
+ * on unsorted edges the histogram bins by a search over an unsorted array.
+ * Any of the three arrays may be NULL (not checked). One small kernel writes
+ * the OR of the failed conditions' bits to *status (int32, device), 0 when
+ * all hold; the caller reads it at its next synchronisation and treats a
+ * non-zero value as SAGE_EINVAL. The Python layer's Store runs it on its
+ * bins once, at construction.
+ * SAGE_EINVAL (nothing enqueued): B outside [1, SAGE_MAX_BINS], Q < 0,
+ * status NULL, misaligned pointers.
+ */
+enum { SAGE_CHECK_EDGES = 1, SAGE_CHECK_REPR = 2, SAGE_CHECK_PROMPT_LEN = 4 };
+int sage_check_inputs(const double* bin_edges, const double* bin_repr, int B, const int32_t* prompt_len, int Q,
+                      int32_t* status, sage_stream_t stream);
+
+/*
+ * sage_debug_theta_floor - test hook, not for production use. Later
+ * sage_predict calls (any thread) raise each query's pre-pass threshold
+ * theta0 to at least `floor` on the filtered (k <= 64) and few-query paths,
+ * which forces queries onto their exact fallback (a query left with fewer
+ * than min(k, N) candidates is answered there); results must not change.
+ * -inf turns it off (the default). SAGE_EINVAL for NaN. Host-only state.
+ */
+int sage_debug_theta_floor(float floor);
 
 /* sage_rank_workspace_bytes - device workspace bytes for sage_rank(Q). */
 size_t sage_rank_workspace_bytes(int Q);

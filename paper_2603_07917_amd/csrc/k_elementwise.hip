@@ -127,6 +127,36 @@ int grid_for(size_t work, int block, int cap = 4096) {
 
 }  // namespace
 
+// Preconditions of the binning and the index scan, checked on the device:
+// edges strictly increasing and finite (the histogram's binary search), the
+// representatives finite, non-negative and non-decreasing, and prompt
+// lengths non-negative (together they make the cost support r (I + r / 2)
+// non-decreasing along a row, which the index scan relies on). One
+// workgroup; bit SAGE_CHECK_* of *status is set for each failed condition,
+// 0 when all hold. Every thread reaches the barrier; thread 0 writes.
+__global__ void __launch_bounds__(1024) check_inputs_kernel(const double* __restrict__ edges, int n_edges,
+                                                            const double* __restrict__ repr, int B,
+                                                            const int32_t* __restrict__ plen, int Q,
+                                                            int32_t* __restrict__ status) {
+  __shared__ int bad;
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  int mine = 0;
+  for (int i = threadIdx.x; edges && i < n_edges; i += blockDim.x) {
+    const double e = edges[i];
+    if (!__builtin_isfinite(e) || (i + 1 < n_edges && !(e < edges[i + 1]))) mine |= 1;
+  }
+  for (int i = threadIdx.x; repr && i < B; i += blockDim.x) {
+    const double r = repr[i];
+    if (!__builtin_isfinite(r) || (i == 0 && !(r >= 0.0)) || (i + 1 < B && !(r <= repr[i + 1]))) mine |= 2;
+  }
+  for (int i = threadIdx.x; plen && i < Q; i += blockDim.x)
+    if (plen[i] < 0) mine |= 4;
+  if (mine) atomicOr(&bad, mine);
+  __syncthreads();
+  if (threadIdx.x == 0) *status = bad;
+}
+
 hipError_t launch_ingest_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream) {
   if (n == 0) return hipSuccess;
   LaunchScope scope("ingest_bf16", stream);
@@ -234,6 +264,12 @@ hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr,
   LaunchScope scope("cost", stream);
   hipLaunchKernelGGL(cost_kernel, dim3(grid_for((size_t)Q * B, 256, 8192)), dim3(256), 0, stream,
                      prompt_len, Q, bin_repr, B, cost);
+  return hipGetLastError();
+}
+
+hipError_t launch_check_inputs(const double* edges, int n_edges, const double* repr, int B, const int32_t* plen,
+                               int Q, int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(check_inputs_kernel, dim3(1), dim3(1024), 0, stream, edges, n_edges, repr, B, plen, Q, status);
   return hipGetLastError();
 }
 

@@ -12,11 +12,15 @@
 // to the query's candidate array with one global atomic per query. The
 // select kernel then folds each query's candidates into its top k.
 //
-// Every true neighbour scores >= theta0, so it is a candidate. A workgroup
-// whose LDS slots for a query fill up (a store with similar rows side by
-// side) sends the rest to the array one atomic at a time; a query whose
-// candidates overflow the array is flagged and answered by the exact list
-// path instead.
+// The pre-pass (stream_sample_kernel) scores its sampled rows with this
+// kernel's own MFMA chain, so theta0 is a score that k distinct rows reach
+// in the search itself, bit for bit: every true neighbour scores >= theta0
+// and is a candidate. A workgroup whose LDS slots for a query fill up (a
+// store with similar rows side by side) sends the rest to the array one
+// atomic at a time; a query whose candidates overflow the array, or that
+// ends with fewer than min(k, N) of them (which the bit-identity above rules
+// out, so only a raised threshold can cause it), is flagged and answered by
+// the exact list path instead.
 #include "sage_device.hpp"
 #include "sage_internal.hpp"
 
@@ -32,6 +36,60 @@ constexpr int kRing = 16;            // k-block loads in flight per wave
 constexpr int kLCap = 64;            // LDS candidate slots per query and workgroup
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Query operands of the 16x16x32 chain, in LDS: slot j * 64 + l holds query
+// l % 16, columns 32 j + 8 (l / 16) .. + 7 (zeros for queries past Q).
+__device__ __forceinline__ void load_query_frags(uint4* qfrag, const EmbView& queries, int Q, int KB) {
+  for (int i = threadIdx.x; i < KB * kWave; i += kThreads) {
+    const int j = i / kWave, l = i % kWave, q = l % 16;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (q < Q) v = *reinterpret_cast<const uint4*>(emb_at(queries, q, 32 * j + 8 * (l / 16)));
+    qfrag[i] = v;
+  }
+}
+
+// Threshold pre-pass of this path: the maximum of each disjoint 16-row group
+// of every sample_every-th 256-row step, gm[q][s][g] (g: the group within
+// the step). A group is scored exactly as the search below scores a tile:
+// d / 32 chained v_mfma_f32_16x16x32_bf16 from a zero accumulator, column
+// blocks in order, row r at operand row r % 16 (tiles start at multiples of
+// 16 in both kernels), query q at operand column q. Each maximum is thus the
+// search's own fp32 score of one row, and the k-th largest of them (theta0)
+// is reached by k distinct rows in the search. Sampled steps are whole.
+__global__ void __launch_bounds__(kThreads) stream_sample_kernel(EmbView queries, int Q, EmbView hist, int N,
+                                                                 int d, int sample_every, int n_samples,
+                                                                 float* __restrict__ gm) {
+  extern __shared__ uint4 qfrag[];                  // d / 32 KiB, sized at launch
+  const int lane = (int)lane_id();
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int KB = d / 32;
+  load_query_frags(qfrag, queries, Q, KB);
+  __syncthreads();
+  const int tile = blockIdx.x * kWaves + w;         // 16 tiles per sampled step
+  if (tile >= n_samples * 16) return;
+  const int s = tile >> 4, g = tile & 15;
+  const int row = min(s * sample_every * 256 + 16 * g + (lane & 15), N - 1);
+  const uint16_t* p = emb_at(hist, row, 8 * (lane >> 4));
+  floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  constexpr int kBatch = 8;                          // loads in flight per wave
+  for (int j0 = 0; j0 < KB; j0 += kBatch) {
+    uint4 a[kBatch];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i)
+      if (j0 + i < KB) a[i] = *reinterpret_cast<const uint4*>(p + (long long)(j0 + i) * hist.panel);
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i)
+      if (j0 + i < KB)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a[i]), as_bf16x8(qfrag[(j0 + i) * kWave + lane]),
+                                                      acc, 0, 0, 0);
+  }
+  // Lane l holds rows 4 (l / 16) .. + 3 of query l % 16: the group maximum
+  // over the lanes l, l ^ 16, l ^ 32, l ^ 48 (exact: no rounding in a max).
+  float m = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3]));
+  m = fmaxf(m, __uint_as_float(xor_lane_u32<16>(__float_as_uint(m))));
+  m = fmaxf(m, __uint_as_float(xor_lane_u32<32>(__float_as_uint(m))));
+  if (lane < Q) gm[((size_t)lane * n_samples + s) * 16 + g] = m;
+}
 
 // Workgroup b scans rows [b * chunk_rows, ...); wave w takes the chunk's
 // 16-row tiles w, w + 4, ... Lane l of a tile: A operand = row l % 16,
@@ -49,12 +107,7 @@ __global__ void __launch_bounds__(kThreads) sim_stream_kernel(
   const int lane = (int)lane_id();
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int KB = d / 32;
-  for (int i = tid; i < KB * kWave; i += kThreads) {
-    const int j = i / kWave, l = i % kWave, q = l % 16;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (q < Q) v = *reinterpret_cast<const uint4*>(emb_at(queries, q, 32 * j + 8 * (l / 16)));
-    qfrag[i] = v;
-  }
+  load_query_frags(qfrag, queries, Q, KB);
   if (tid < kStreamMaxQ) lcnt[tid] = 0;
   const int ql = lane & 15;
   const float thr = ql < Q ? float_below(theta0[ql]) : __builtin_inff();
@@ -196,15 +249,17 @@ __device__ __forceinline__ void list_fold(uint64_t (&lv)[S], uint64_t key) {
   list_clean<S>(lv);
 }
 
-// One workgroup of 16 waves per query. Wave w takes candidates
+// One workgroup of 16 waves per query; a query with more candidates than the
+// array holds, or fewer than min(k, N), is flagged for the exact path and
+// left untouched. Wave w takes candidates
 // 64 w + lane + 1024 i; keys that beat its list's last key are gathered in
 // LDS and folded 64 at a time. The 16 lists are then merged pairwise in a
 // tree, and wave 0 writes the first k.
 template <int S>
 __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __restrict__ cand,
                                                           const int* __restrict__ cand_count, int cap, int k,
-                                                          int* __restrict__ flags, int32_t* __restrict__ ids,
-                                                          float* __restrict__ sims) {
+                                                          int need, int* __restrict__ flags,
+                                                          int32_t* __restrict__ ids, float* __restrict__ sims) {
   constexpr int KL = 64 * S;
   constexpr int W = 16;
   __shared__ uint64_t lists[W][KL];
@@ -214,7 +269,7 @@ __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __rest
   const int lane = (int)lane_id();
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int n = cand_count[q];
-  if (n > cap) {
+  if (n > cap || n < need) {                         // need = min(k, N)
     if (tid == 0) flags[q] = 1;
     return;
   }
@@ -285,6 +340,18 @@ __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __rest
 
 }  // namespace
 
+hipError_t launch_stream_sample(EmbView queries, int Q, EmbView hist, int N, int d, int sample_every,
+                                int n_samples, float* gm, hipStream_t stream) {
+  if (Q <= 0 || Q > kStreamMaxQ || d % 32 != 0 || d > kStreamMaxD || n_samples <= 0 || sample_every <= 0 ||
+      (long long)(n_samples - 1) * sample_every * 256 + 256 > N)
+    return hipErrorInvalidValue;
+  const int blocks = (n_samples * 16 + kWaves - 1) / kWaves;
+  const size_t lds = (size_t)(d / 32) * kWave * sizeof(uint4);
+  hipLaunchKernelGGL(stream_sample_kernel, dim3(blocks), dim3(kThreads), lds, stream, queries, Q, hist, N, d,
+                     sample_every, n_samples, gm);
+  return hipGetLastError();
+}
+
 hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int d, int k, int chunk_rows,
                                 const float* theta0, int cap, uint64_t* cand, int* cand_count, int* flags,
                                 int32_t* ids, float* sims, hipStream_t stream) {
@@ -299,14 +366,14 @@ hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int
   }
   LaunchScope scope("topk_select", stream);
   if (k <= 64)
-    hipLaunchKernelGGL((select_few_kernel<1>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k, flags,
-                       ids, sims);
+    hipLaunchKernelGGL((select_few_kernel<1>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
+                       min(k, N), flags, ids, sims);
   else if (k <= 128)
-    hipLaunchKernelGGL((select_few_kernel<2>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k, flags,
-                       ids, sims);
+    hipLaunchKernelGGL((select_few_kernel<2>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
+                       min(k, N), flags, ids, sims);
   else
-    hipLaunchKernelGGL((select_few_kernel<4>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k, flags,
-                       ids, sims);
+    hipLaunchKernelGGL((select_few_kernel<4>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
+                       min(k, N), flags, ids, sims);
   return hipGetLastError();
 }
 

@@ -897,10 +897,11 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
 // sorted (wave bitonic sort) and folded in with C_i = max(A_i, B_{63-i}) and
 // six half-cleaner stages. Wave 0 then folds in
 // the other three lists and writes the first k. A query with an overflowed
-// segment is flagged for the exact fallback and left untouched here.
+// segment, or with fewer than min(k, N) candidates in all, is flagged for
+// the exact fallback and left untouched here.
 __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict__ seg,
                                                      const int* __restrict__ seg_count, int n_chunks,
-                                                     int seg_cap, int k, int* __restrict__ flags,
+                                                     int seg_cap, int k, int need, int* __restrict__ flags,
                                                      int32_t* __restrict__ ids, float* __restrict__ sims) {
   __shared__ int off[kWave + 1];
   __shared__ int over;
@@ -921,7 +922,10 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
     }
     off[lane] = incl - c;
     if (lane == kWave - 1) off[kWave] = incl;
-    const bool ov = __any(n > seg_cap);
+    // Flag the query when a segment overflowed, or when fewer than
+    // min(k, N) keys beat theta0: the pre-pass scores are the filter's own,
+    // bit for bit, so the latter only follows from a raised threshold.
+    const bool ov = __any(n > seg_cap) || __shfl(incl, kWave - 1, kWave) < need;
     if (lane == 0) over = ov ? 1 : 0;
   }
   __syncthreads();
@@ -1010,21 +1014,35 @@ hipError_t launch_lists(EmbView queries, int Q, EmbView hist, int N, int d, int 
   return hipGetLastError();
 }
 
+// Which kernel scores the sampled steps: each search path samples with the
+// arithmetic of its own search, so the sampled scores are the search's own.
+enum class Sampler { ring, list, stream };
+
+// Threshold floor for tests of the exact fallback (sage_debug_theta_floor):
+// theta0 = max(theta0, floor) before the search.
+__global__ void theta_floor_kernel(float* __restrict__ theta0, int Q, float floor) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < Q) theta0[q] = fmaxf(theta0[q], floor);
+}
+
 hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int k,
-                        const SimTopkPlan& p, int q_tiles, bool big, float* gm, float* theta0,
+                        const SimTopkPlan& p, int q_tiles, Sampler sampler, float* gm, float* theta0,
                         int* clear, hipStream_t stream) {
   {
     LaunchScope scope("threshold_sample", stream);
     const dim3 grid(q_tiles, p.n_samples);
-    if (big) {
+    if (sampler == Sampler::stream) {
+      const hipError_t e = launch_stream_sample(queries, Q, hist, N, d, p.sample_every, p.n_samples, gm, stream);
+      if (e != hipSuccess) return e;
+    } else if (sampler == Sampler::ring) {
       const int spb = p.f_spb;
       const dim3 rgrid(q_tiles, (p.n_samples + spb - 1) / spb);
       hipLaunchKernelGGL(threshold_sample_ring_kernel, rgrid, dim3(kThreads), 0, stream, queries, Q,
                          hist, N, d, p.sample_every, p.n_samples, spb, gm);
-    } else if (p.list_len == 128 && !p.stream) {
+    } else if (p.list_len == 128) {              // the same core as sim_topk_kernel<2, 128>
       hipLaunchKernelGGL((threshold_sample_kernel<2>), grid, dim3(kThreads), 0, stream, queries, Q,
                          hist, N, d, p.sample_every, p.n_samples, gm);
-    } else {
+    } else {                                     // the same core as sim_topk_kernel<1, 256>
       hipLaunchKernelGGL((threshold_sample_kernel<1>), grid, dim3(kThreads), 0, stream, queries, Q,
                          hist, N, d, p.sample_every, p.n_samples, gm);
     }
@@ -1047,6 +1065,9 @@ hipError_t launch_theta(EmbView queries, int Q, EmbView hist, int N, int d, int 
     else
       hipLaunchKernelGGL((threshold_select_kernel<128, 1>), grid, dim3(256), 0, stream, gm, Q, m, k, theta0, clear);
   }
+  const float floor = debug_theta_floor();
+  if (sampler != Sampler::list && floor > -__builtin_inff())   // only the paths with a guarded fallback
+    hipLaunchKernelGGL(theta_floor_kernel, dim3((Q + 255) / 256), dim3(256), 0, stream, theta0, Q, floor);
   return hipGetLastError();
 }
 
@@ -1159,7 +1180,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
   hipError_t e;
   if (p.fast) {
     if (p.n_samples > 0) {
-      e = launch_theta(queries, Q, hist, N, d, k, p, p.f_q_tiles, true, gm, theta0, nullptr, stream);
+      e = launch_theta(queries, Q, hist, N, d, k, p, p.f_q_tiles, Sampler::ring, gm, theta0, nullptr, stream);
       if (e != hipSuccess) return e;
     }
     uint64_t* seg = reinterpret_cast<uint64_t*>(ws + p.off_seg);
@@ -1174,7 +1195,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     {
       LaunchScope scope("topk_select", stream);
       hipLaunchKernelGGL(select_kernel, dim3(Q), dim3(256), 0, stream, seg, segcnt,
-                         p.f_n_chunks, p.seg_cap, k, flags, ids, sims);
+                         p.f_n_chunks, p.seg_cap, k, min(k, N), flags, ids, sims);
     }
     // Exact fallback for queries whose candidates overflowed (no work otherwise).
     e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
@@ -1185,7 +1206,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     uint64_t* cand = reinterpret_cast<uint64_t*>(ws + p.off_cand);
     int* ccount = reinterpret_cast<int*>(ws + p.off_ccount);
     int* flags = reinterpret_cast<int*>(ws + p.off_flags);
-    e = launch_theta(queries, Q, hist, N, d, k, p, 1, false, gm, theta0, ccount, stream);
+    e = launch_theta(queries, Q, hist, N, d, k, p, 1, Sampler::stream, gm, theta0, ccount, stream);
     if (e != hipSuccess) return e;
     e = launch_stream_search(queries, Q, hist, N, d, k, p.s_chunk_rows, theta0, p.s_cap, cand, ccount, flags,
                              ids, sims, stream);
@@ -1198,7 +1219,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, merge_lists, ids, sims, stream);
   }
   if (p.n_samples > 0) {
-    e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, false, gm, theta0, nullptr, stream);
+    e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, Sampler::list, gm, theta0, nullptr, stream);
     if (e != hipSuccess) return e;
   }
   const float* th = p.n_samples > 0 ? theta0 : nullptr;

@@ -2,6 +2,7 @@
 // dispatch to the gfx950 kernels. Nothing here allocates device memory.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -214,7 +215,7 @@ SAGE_API int sage_ingest_bf16(const float* src, size_t n, uint16_t* dst, sage_st
 namespace {
 int check_panels_args(const char* fn, const void* src, int rows, int d, const void* dst) {
   if (rows < 0) return fail(SAGE_EINVAL, "%s: rows=%d is negative", fn, rows);
-  if (rows > (1 << 29)) return fail(SAGE_EINVAL, "%s: rows=%d above 2^29", fn, rows);
+  if (rows >= (1 << 29)) return fail(SAGE_EINVAL, "%s: rows=%d not below 2^29", fn, rows);
   if (d < 32 || d % 32 != 0) return fail(SAGE_EINVAL, "%s: d=%d must be a positive multiple of 32", fn, d);
   if (rows == 0) return SAGE_OK;
   if (!src || !dst) return fail(SAGE_EINVAL, "%s: NULL pointer", fn);
@@ -528,6 +529,44 @@ SAGE_API int sage_index_attained_table(const float* mass, const int32_t* prompt_
   return hip_status(sage::launch_index(mass, nullptr, prompt_len, bin_repr, nullptr, bucket, Q, B, index, nullptr,
                                        (hipStream_t)stream, &table),
                     "index table launch");
+}
+
+// --------------------------------------------------------- input check
+SAGE_API int sage_check_inputs(const double* bin_edges, const double* bin_repr, int B, const int32_t* prompt_len,
+                               int Q, int32_t* status, sage_stream_t stream) {
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (!status) return fail(SAGE_EINVAL, "sage_check_inputs: status is NULL");
+  const void* ptrs[] = {bin_edges, bin_repr, prompt_len, status};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(SAGE_EINVAL, "sage_check_inputs: misaligned pointer");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_check_inputs(bin_edges, B + 1, bin_repr, B, prompt_len, Q, status,
+                                              (hipStream_t)stream),
+                    "check_inputs launch");
+}
+
+// ---------------------------------------------------------- test hook
+namespace {
+std::atomic<uint32_t> g_theta_floor_bits{0xff800000u};   // -inf: off
+}  // namespace
+
+namespace sage {
+float debug_theta_floor() {
+  const uint32_t b = g_theta_floor_bits.load(std::memory_order_relaxed);
+  float f;
+  std::memcpy(&f, &b, sizeof f);
+  return f;
+}
+}  // namespace sage
+
+SAGE_API int sage_debug_theta_floor(float floor) {
+  if (std::isnan(floor)) return fail(SAGE_EINVAL, "sage_debug_theta_floor: NaN");
+  uint32_t b;
+  std::memcpy(&b, &floor, sizeof b);
+  g_theta_floor_bits.store(b, std::memory_order_relaxed);
+  return ok();
 }
 
 // ----------------------------------------------------------------- rank

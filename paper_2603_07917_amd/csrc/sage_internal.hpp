@@ -67,6 +67,12 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k);
 // Few-query stream path: limits, and the search + candidate select.
 constexpr int kStreamMaxQ = 16;
 constexpr int kStreamMaxD = 2048;
+// Threshold pre-pass of the stream path (group maxima of the sampled steps).
+hipError_t launch_stream_sample(EmbView queries, int Q, EmbView hist, int N, int d, int sample_every,
+                                int n_samples, float* gm, hipStream_t stream);
+// Test hook (sage_debug_theta_floor): a floor on the pre-pass threshold of the
+// filtered and stream paths; -inf when unset.
+float debug_theta_floor();
 hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int d, int k, int chunk_rows,
                                 const float* theta0, int cap, uint64_t* cand, int* cand_count, int* flags,
                                 int32_t* ids, float* sims, hipStream_t stream);
@@ -84,6 +90,9 @@ hipError_t launch_queue_admit(const int64_t* free_slots, int batch, const float*
                               int32_t* plen, int64_t* request, hipStream_t stream);
 hipError_t launch_queue_dispatch(const int32_t* order, int batch, const int64_t* request, int slots,
                                  int64_t* free_slots, int64_t* dispatched, hipStream_t stream);
+// Device check of the bin and prompt-length preconditions (bitmask to *status).
+hipError_t launch_check_inputs(const double* edges, int n_edges, const double* repr, int B, const int32_t* plen,
+                               int Q, int32_t* status, hipStream_t stream);
 hipError_t launch_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B,
                        float* cost, hipStream_t stream);
 hipError_t launch_mix_uniform(const float* mass, int Q, int B, float weight, float* out,

@@ -55,6 +55,8 @@ def load_library():
         "sage_rank": (I, [P, I, P, P, Z, S]),
         "sage_simulate": (I, [P, P, P, I, P, I, I, I, I, ctypes.c_double, I, P, P]),
         "sage_mix_uniform": (I, [P, I, I, F, P, S]),
+        "sage_check_inputs": (I, [P, P, I, P, I, P, S]),
+        "sage_debug_theta_floor": (I, [F]),
         "sage_status_string": (ctypes.c_char_p, [I]),
         "sage_last_error": (ctypes.c_char_p, []),
         "sage_timer_create": (I, [I, ctypes.POINTER(P)]),
@@ -365,6 +367,50 @@ def simulate(arrival, prompt_len, output_len, order, *, rate: float, servers: in
     return finish, pre
 
 
+CHECK_BITS = {1: "bin edges not finite and strictly increasing",
+              2: "bin representatives not finite, non-negative and non-decreasing",
+              4: "negative prompt length"}
+
+
+def check_inputs(bin_edges: Optional[torch.Tensor] = None, bin_repr: Optional[torch.Tensor] = None,
+                 prompt_len: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+                 sync: bool = True):
+    """Device check of the bin and prompt-length preconditions
+    (sage_check_inputs). With `sync`, waits for the result and raises
+    SageError naming each failed condition; otherwise returns the int32
+    status tensor for the caller to read later."""
+    if bin_edges is None and bin_repr is None:
+        raise SageError("check_inputs needs bin_edges or bin_repr (they give B)")
+    if bin_edges is not None:
+        _dev(bin_edges, torch.float64, "bin_edges", 1)
+    if bin_repr is not None:
+        _dev(bin_repr, torch.float64, "bin_repr", 1)
+    B = bin_edges.shape[0] - 1 if bin_edges is not None else bin_repr.shape[0]
+    if bin_edges is not None and bin_repr is not None and bin_repr.shape[0] != B:
+        raise SageError("bin_repr must have one entry per bin (len(bin_edges) - 1)")
+    Q = 0
+    if prompt_len is not None:
+        _dev(prompt_len, torch.int32, "prompt_len", 1)
+        Q = prompt_len.shape[0]
+    dev_ = (bin_edges if bin_edges is not None else bin_repr).device
+    if status is None:
+        status = torch.empty(4, dtype=torch.int32, device=dev_)
+    _check(load_library().sage_check_inputs(_ptr(bin_edges), _ptr(bin_repr), B, _ptr(prompt_len), Q,
+                                            _ptr(status), _stream()))
+    if not sync:
+        return status
+    bits = int(status[0].item())
+    if bits:
+        raise SageError("SAGE_EINVAL: " + "; ".join(v for b, v in CHECK_BITS.items() if bits & b))
+    return status
+
+
+def debug_theta_floor(floor: float):
+    """Test hook: raise the pre-pass threshold of later predict calls to at
+    least `floor` (-inf: off), forcing queries onto the exact fallback."""
+    _check(load_library().sage_debug_theta_floor(float(floor)))
+
+
 class Store:
     """A resident history store plus reusable device workspaces.
 
@@ -386,6 +432,7 @@ class Store:
         self.hist_len = hist_len
         self.bin_edges = bin_edges
         self.bin_repr = bin_repr
+        check_inputs(bin_edges, bin_repr)              # once per store: the bins' order
         self.k = int(k)
         self.tau = float(tau)
         self._ws = torch.empty(16, dtype=torch.uint8, device=hist_emb.device)

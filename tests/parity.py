@@ -184,3 +184,18 @@ def check_sorted_stably(order, g):
     v = np.asarray(g)[order]
     ok = (v[:-1] < v[1:]) | ((v[:-1] == v[1:]) & (order[:-1] < order[1:]))
     assert np.all(ok), "order is not a stable ascending sort of its keys"
+
+
+def check_rank_vs_oracle(order, G_o, rtol=INDEX_RTOL):
+    """A rank output against the oracle's index values G_o of the same rows:
+    two requests may come out of the oracle's order only when their values
+    are within rtol relative of each other, i.e. along the GPU's order every
+    value is at least the largest one before it, shrunk by rtol (+inf rows
+    last)."""
+    v = np.asarray(G_o, dtype=np.float64)[np.asarray(order)]
+    fin = np.isfinite(v)
+    n_fin = int(fin.sum())
+    assert np.all(fin[:n_fin]) and not np.any(fin[n_fin:]), "+inf rows are not last"
+    run = np.maximum.accumulate(v[:n_fin])
+    bad = v[:n_fin] < run * (1.0 - rtol) - 1e-300
+    assert not bad.any(), f"order departs from the oracle's beyond {rtol} relative at {np.nonzero(bad)[0][:5]}"

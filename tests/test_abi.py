@@ -226,3 +226,27 @@ def test_index_rank_cost_hist_validation(lib):
     assert lib.sage_ingest_bf16(None, 10, A, None) == SAGE_EINVAL
     assert lib.sage_ingest_bf16(A, 100, A + 16, None) == SAGE_EINVAL     # overlap
     assert lib.sage_ingest_bf16(None, 0, None, None) == SAGE_OK
+
+
+def test_check_inputs_and_debug_hook_validation(lib):
+    fn = lib.sage_check_inputs
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                   ctypes.c_void_p, ctypes.c_void_p]
+    a = [A + 0x1000 * i for i in range(4)]
+    assert fn(a[0], a[1], 0, a[2], 4, a[3], None) == SAGE_EINVAL          # B
+    assert fn(a[0], a[1], 5000, a[2], 4, a[3], None) == SAGE_EINVAL       # B
+    assert fn(a[0], a[1], 16, a[2], -1, a[3], None) == SAGE_EINVAL        # Q
+    assert fn(a[0], a[1], 16, a[2], 4, None, None) == SAGE_EINVAL         # status
+    assert fn(a[0] + 8, a[1], 16, a[2], 4, a[3], None) == SAGE_EINVAL     # misaligned
+    assert fn(a[0], a[1], 16, a[2] + 4, 4, a[3], None) == SAGE_EINVAL
+    hook = lib.sage_debug_theta_floor
+    hook.argtypes = [ctypes.c_float]
+    assert hook(math.nan) == SAGE_EINVAL
+    assert hook(-math.inf) == SAGE_OK                                      # off (the default)
+
+
+def test_panels_ingest_rejects_rows_at_2_pow_29(lib):
+    # rows * 4 pieces must fit in int32 inside the kernels
+    for fn in (lib.sage_ingest_bf16_panels, lib.sage_panels_from_rows):
+        assert fn(A, 1 << 29, 32, A + (1 << 40), None) == SAGE_EINVAL
+        assert b"2^29" in lib.sage_last_error()

@@ -197,35 +197,67 @@ def test_config1_end_to_end():
     print(f"config 1: {clean}/{spec.Q} queries compared through the index", flush=True)
 
 
-def test_config2_full_size_sampled():
-    """The benchmark's workload and launch configuration; sampled queries checked."""
+def check_decision_blocked(w, rows, out, block):
+    """check_decision over `rows` in blocks of queries (bounded score rows),
+    the store widened to fp64 once; also the order against the oracle's
+    index of the GPU's own masses. Returns the number of clean rows."""
+    ids, sims, counts, mass, g, order = out
+    spec = w.spec
+    hf = oracle.bf16_to_f64(oracle.round_to_bf16(w.hist_emb))
+    clean = 0
+    for s0 in range(0, len(rows), block):
+        r = rows[s0:s0 + block]
+        S = oracle.similarity(oracle.round_to_bf16(w.queries[r]), hf)
+        c, mass_o, delta = parity.check_predict(ids[r], sims[r], counts[r], mass[r], S, w.hist_len,
+                                                w.bin_edges, spec.tau, spec.k)
+        x = oracle.cost(w.prompt_len[r], w.bin_repr)
+        parity.check_index_downstream(g[r], mass_o, x, delta, np.nonzero(c)[0])
+        clean += int(c.sum())
+        print(f"  rows {s0}..{s0 + len(r)}: {int(c.sum())} clean", flush=True)
+    parity.check_sorted_stably(order, g)
+    # cost + index on the GPU's own masses (identical inputs), then the order
+    G_o = parity.check_index(g, mass, oracle.cost(w.prompt_len, w.bin_repr))
+    parity.check_rank_vs_oracle(order, G_o)
+    return clean
+
+
+def run_decision(w):
+    spec = w.spec
+    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
+                       spec.k, spec.tau)
+    out = store.decide(dev(w.queries), dev(w.prompt_len))
+    return [host(t) for t in out]
+
+
+@pytest.mark.timeout(900)
+def test_config2_full_size_every_query():
+    """The mid workload (4,096 queries, 262,144 rows, d = 768) at full size
+    in the benchmark's launch configuration; every query checked."""
     w = workloads.make_config(2)
-    spec = w.spec
-    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
-                       spec.k, spec.tau)
-    out = store.decide(dev(w.queries), dev(w.prompt_len))
-    ids, sims, counts, mass, g, order = [host(t) for t in out]
-    rng = np.random.default_rng(2)
-    rows = np.sort(rng.choice(spec.Q, size=48, replace=False))
-    rows = np.unique(np.concatenate([rows, [0, spec.Q - 1]]))
-    clean = check_decision(w, rows, ids, sims, counts, mass, g, order, spec.k, spec.tau)
-    print(f"config 2: {clean}/{len(rows)} sampled queries compared through the index", flush=True)
+    out = run_decision(w)
+    rows = np.arange(w.spec.Q)
+    clean = check_decision_blocked(w, rows, out, 512)
+    print(f"config 2: {clean}/{len(rows)} queries compared through the index", flush=True)
 
 
+@pytest.mark.timeout(900)
 def test_config3_full_size_sampled():
-    """The GEMM-bound workload (1M rows, d = 1024, 10% noise rows and queries), sampled."""
+    """The GEMM-bound workload (16,384 queries, 1M rows, d = 1024, 10% noise
+    rows and queries) at full size: a seeded sample of 2,048 queries holding
+    every noise query (they exercise the tau fallback), the first and last
+    query, and the rest drawn uniformly."""
     w = workloads.make_config(3)
-    spec = w.spec
-    store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
-                       spec.k, spec.tau)
-    out = store.decide(dev(w.queries), dev(w.prompt_len))
-    ids, sims, counts, mass, g, order = [host(t) for t in out]
-    rng = np.random.default_rng(3)
+    Q = w.spec.Q
+    out = run_decision(w)
     noise_q = np.nonzero(w.query_cluster < 0)[0]
-    rows = np.concatenate([rng.choice(spec.Q, size=20, replace=False), noise_q[:4], [0, spec.Q - 1]])
-    rows = np.unique(rows)
-    clean = check_decision(w, rows, ids, sims, counts, mass, g, order, spec.k, spec.tau)
-    print(f"config 3: {clean}/{len(rows)} sampled queries compared through the index", flush=True)
+    rng = np.random.default_rng(3)
+    rest = np.setdiff1d(np.arange(Q), np.concatenate([noise_q, [0, Q - 1]]))
+    n_more = max(0, 2048 - len(noise_q) - 2)
+    rows = np.unique(np.concatenate([noise_q, [0, Q - 1], rng.choice(rest, size=n_more, replace=False)]))
+    assert len(rows) == max(2048, len(noise_q) + 2) and np.isin(noise_q, rows).all()
+    clean = check_decision_blocked(w, rows, out, 256)
+    print(f"config 3: {clean}/{len(rows)} sampled queries ({len(noise_q)} noise) compared through the index",
+          flush=True)
 
 
 def test_stream_path_clustered_store():

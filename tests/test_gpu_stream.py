@@ -1,8 +1,10 @@
 """The streaming workload end to end: a standing queue of 8,192 requests over
 the 4M-row store; each decision admits 8 new requests, re-indexes all 8,200,
-ranks them and dispatches 8. The new requests are checked against the
-oracle's own predictions and indices on a few decisions; the queue mechanics
-(slot refills, re-index, stable rank) by their properties."""
+ranks them and dispatches 8. The queue is driven through all 1,024 decisions;
+at decisions 0, 1, 511, 1023 and 12 seeded others the new requests are
+checked against the oracle's own predictions and indices, and the whole
+queue's index and order against the oracle's on the queue's masses. The
+dispatch bookkeeping is checked at every decision."""
 import numpy as np
 import pytest
 import torch
@@ -31,49 +33,70 @@ def oracle_rows(queries_f32, hist_f32, block=1 << 18):
     return np.concatenate(parts, axis=1)
 
 
+def checked_calls(n_calls, seed=5, extra=12):
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, n_calls // 2 - 1, n_calls - 1]
+    others = rng.choice(np.setdiff1d(np.arange(n_calls), fixed), size=extra, replace=False)
+    return sorted(set(fixed) | set(int(c) for c in others))
+
+
+@pytest.mark.timeout(900)
 def test_streaming_decisions_vs_oracle():
     spec = workloads.CONFIGS[5]
     batch, standing = 8, 8192
+    n_calls = spec.Q // batch                          # 1,024 decisions of 8 arrivals
     w = workloads.make_config(5)
     sq, splen = workloads.make_standing(spec, 5, standing)
-    print("workload generated", flush=True)
+    check = checked_calls(n_calls)
+    assert {0, 1, 511, 1023} <= set(check) and len(check) == 16
+    # the oracle's score rows of every checked decision's arrivals, computed up front
+    sel = np.concatenate([np.arange(c * batch, (c + 1) * batch) for c in check])
+    S_all = oracle_rows(w.queries[sel], w.hist_emb)
+    print(f"workload generated; oracle rows for decisions {check}", flush=True)
     store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr),
                        spec.k, spec.tau)
     _, _, _, smass = store.predict(dev(sq))
     queue = sage.Queue(store, smass.clone(), dev(splen), batch)
     requests = list(range(standing))                  # queued request ids in slot order
-    for call in range(3):
+    x_all = None
+    for call in range(n_calls):
         a = call * batch
         q_new = w.queries[a:a + batch]
         p_new = w.prompt_len[a:a + batch]
         free_before = host(queue.free).copy()
         (ids, sims, counts, mass), dispatched = queue.decide(dev(q_new), dev(p_new))
+        order = host(queue.order)
+        for j, slot in enumerate(free_before):
+            if slot >= len(requests):
+                requests.append(None)
+            requests[slot] = standing + a + j
+        want = [requests[s] for s in order[:batch]]
+        assert list(host(dispatched)) == want, f"dispatch, decision {call}"
+        assert np.array_equal(host(queue.free), order[:batch])
+        if call not in check:
+            continue
         ids, sims, counts, mass = host(ids), host(sims), host(counts), host(mass)
+        i = check.index(call)
+        S = S_all[i * batch:(i + 1) * batch]
         # the new requests' predictions against the oracle's own
-        S = oracle_rows(q_new, w.hist_emb)
         clean, mass_o, delta = parity.check_predict(ids, sims, counts, mass, S, w.hist_len,
                                                     w.bin_edges, spec.tau, spec.k)
         # they went into the freed slots
         qmass, qplen = host(queue.mass), host(queue.prompt_len)
         assert np.array_equal(qmass[free_before], mass)
         assert np.array_equal(qplen[free_before], p_new)
-        g, order = host(queue.index), host(queue.order)
+        g = host(queue.index)
         # the new requests' index against the oracle's, from the oracle's masses
         parity.check_index_downstream(g[free_before], mass_o, oracle.cost(p_new, w.bin_repr), delta,
                                       np.nonzero(clean)[0])
-        # every slot was re-indexed from the queue's current masses, then ranked stably
+        # the whole queue: index on its own masses (identical inputs), then the order
+        G_o = parity.check_index(g, qmass, oracle.cost(qplen, w.bin_repr))
+        parity.check_sorted_stably(order, g)
+        parity.check_rank_vs_oracle(order, G_o)
+        # every slot was re-indexed from the queue's current masses
         g_again = host(sage.index(queue.mass, queue.prompt_len, store.bin_repr))
         assert np.array_equal(g.view(np.uint32), g_again.view(np.uint32))
-        parity.check_sorted_stably(order, g)
-        # dispatch: the first `batch` slots of the order, by request id
-        for j, slot in enumerate(free_before):
-            if slot >= len(requests):
-                requests.append(None)
-            requests[slot] = standing + a + j
-        want = [requests[s] for s in order[:batch]]
-        assert list(host(dispatched)) == want
-        assert np.array_equal(host(queue.free), order[:batch])
-        print(f"call {call}: {int(clean.sum())}/{batch} rows compared through the index; "
+        print(f"decision {call}: {int(clean.sum())}/{batch} rows compared through the index; "
               f"dispatched {want}", flush=True)
 
 
