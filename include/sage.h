@@ -187,6 +187,31 @@ int sage_predict_layout(const uint16_t* queries, int query_layout, int Q,
                         void* workspace, size_t workspace_bytes, sage_stream_t stream);
 
 /*
+ * sage_predict_noalloc - sage_predict_layout for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same search with no workspace
+ * argument. Its scratch memory is a static device array of
+ * SAGE_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held until the
+ * process ends; the call allocates and frees nothing. Inputs and outputs are
+ * the caller's, as in sage_predict_layout, and the outputs are identical to
+ * that call's.
+ *   SAGE_EWORKSPACE (nothing enqueued) when the search needs more scratch
+ *   than the array holds: sage_predict_workspace_bytes(Q, N, d, k, B) must
+ *   not exceed SAGE_NOALLOC_SCRATCH_BYTES (few-query decisions against a
+ *   store of millions of rows fit; so do batches of a few hundred queries).
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (other streams, other host threads) race and must be ordered by
+ * the caller. Nothing in the array needs to start cleared: each call writes
+ * every scratch value before reading it.
+ */
+#define SAGE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int sage_predict_noalloc(const uint16_t* queries, int query_layout, int Q,
+                         const uint16_t* hist_emb, int hist_layout, const int32_t* hist_len, int N, int d,
+                         int k, float tau, const double* bin_edges, int B,
+                         int32_t* nbr_ids, float* nbr_sims, int32_t* counts, float* mass,
+                         sage_stream_t stream);
+
+/*
  * sage_histogram - the predicted output-length distribution alone (the last
  * stage of sage_predict, Sec. 3.1), for neighbour lists obtained elsewhere.
  *   nbr_ids [Q, k] int32 history indices; entries outside [0, N) mean "no

@@ -361,6 +361,55 @@ SAGE_API int sage_predict_layout(const uint16_t* queries, int query_layout, int 
   return hip_status(e, "hist launch");
 }
 
+// ------------------------------------------------ predict, no allocation
+// Workspace of sage_predict_noalloc: a file-scope device array, one copy per
+// GPU, held until the process ends. Host code never passes its name to a
+// kernel (on the host the name is only a stand-in); it uses the device
+// address from hipGetSymbolAddress, looked up once per device with that
+// device current.
+static __device__ __align__(256) unsigned char scratch[SAGE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+int scratch_address(void** out) {
+  static std::mutex mu;
+  static std::vector<void*> addr;                    // per device ordinal, NULL until looked up
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SAGE_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)addr.size() <= dev) addr.resize(dev + 1, nullptr);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SAGE_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return SAGE_OK;
+}
+}  // namespace
+
+SAGE_API int sage_predict_noalloc(const uint16_t* queries, int query_layout, int Q, const uint16_t* hist_emb,
+                                  int hist_layout, const int32_t* hist_len, int N, int d, int k, float tau,
+                                  const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,
+                                  int32_t* counts, float* mass, sage_stream_t stream) {
+  int st = check_predict_sizes(Q, N, d, k, B);
+  if (st != SAGE_OK) return st;
+  if (Q == 0) return sage_predict_layout(queries, query_layout, 0, hist_emb, hist_layout, hist_len, N, d, k, tau,
+                                         bin_edges, B, nbr_ids, nbr_sims, counts, mass, nullptr, 0, stream);
+  const size_t need = sage::plan_sim_topk(Q, N, d, k).workspace_bytes();
+  if (need > (size_t)SAGE_NOALLOC_SCRATCH_BYTES)
+    return fail(SAGE_EWORKSPACE, "sage_predict_noalloc: this search needs %zu bytes of scratch, the static "
+                "array holds %zu (use sage_predict_layout with a workspace)", need,
+                (size_t)SAGE_NOALLOC_SCRATCH_BYTES);
+  if ((st = check_device()) != SAGE_OK) return st;
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws)) != SAGE_OK) return st;
+  return sage_predict_layout(queries, query_layout, Q, hist_emb, hist_layout, hist_len, N, d, k, tau, bin_edges, B,
+                             nbr_ids, nbr_sims, counts, mass, ws, (size_t)SAGE_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_emb,
                           const int32_t* hist_len, int N, int d, int k, float tau,
                           const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,

@@ -56,6 +56,7 @@ def load_library():
         "sage_simulate": (I, [P, P, P, I, P, I, I, I, I, ctypes.c_double, I, P, P]),
         "sage_mix_uniform": (I, [P, I, I, F, P, S]),
         "sage_check_inputs": (I, [P, P, I, P, I, P, S]),
+        "sage_predict_noalloc": (I, [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, S]),
         "sage_debug_theta_floor": (I, [F]),
         "sage_status_string": (ctypes.c_char_p, [I]),
         "sage_last_error": (ctypes.c_char_p, []),

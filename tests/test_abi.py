@@ -250,3 +250,14 @@ def test_panels_ingest_rejects_rows_at_2_pow_29(lib):
     for fn in (lib.sage_ingest_bf16_panels, lib.sage_panels_from_rows):
         assert fn(A, 1 << 29, 32, A + (1 << 40), None) == SAGE_EINVAL
         assert b"2^29" in lib.sage_last_error()
+
+
+def test_predict_noalloc_rejects_before_enqueue(lib):
+    fn = lib.sage_predict_noalloc
+    P, I, F = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+    fn.argtypes = [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, P]
+    # a search needing more scratch than the static array: SAGE_EWORKSPACE, before any device call
+    assert fn(A, 1, 4096, A, 1, A, 262144, 768, 64, 0.8, A, 256, A, A, A, A, None) == SAGE_EWORKSPACE
+    assert b"static" in lib.sage_last_error()
+    assert fn(A, 1, 4, A, 1, A, 100, 48, 8, 0.8, A, 16, A, A, A, A, None) == SAGE_EINVAL      # d % 32
+    assert fn(A, 1, 4, A, 1, A, 100, 64, 0, 0.8, A, 16, A, A, A, A, None) == SAGE_EINVAL      # k
