@@ -831,6 +831,57 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
   auto epi = [&](floatx16 (&acc)[4][4], int h0, int step_end) {
     const int lim = step_end - h0 - 128 * wh - 4 * half;     // r(i) < lim: row inside the step
     const int hl = h0 + 128 * wh + 4 * half;
+    // Rows inside the step: all of them but in a sweep's last, partial step,
+    // where r(i) grows with i, so they are the lowest bits (bits 4g..4g+3 are
+    // rows 8g..8g+3, hence the count below).
+    uint64_t in_step = ~0ull;
+    if (step_end - h0 < kStepRows) {
+      const int c = min(max(lim, 0), 128);
+      const int n_in = 4 * (c >> 3) + min(c & 7, 4);
+      in_step = n_in >= 64 ? ~0ull : (1ull << n_in) - 1ull;
+    }
+    // Column t's survivors are written one column later, so that its LDS
+    // atomic (the segment position) is in flight during the next column's
+    // compare. Per tile, the lane's first survivor is picked from the
+    // registers by a select tree on its index; a lane with two or more
+    // survivors in one tile (rare) takes the rest through its LDS row.
+    uint64_t m_prev = 0;
+    int base_prev = 0;
+    uint32_t f_prev = 0;
+    float fv_prev[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    auto write_column = [&](int t, uint64_t m, int base, uint32_t fidx, const float (&fv)[4]) {
+      const int ql = 128 * wq + 32 * t + l32;
+      uint64_t* dst = seg + ((size_t)(q0 + ql) * n_chunks + chunk) * seg_cap;
+      uint64_t rest = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t bits = (uint32_t)(m >> (16 * u)) & 0xffffu;
+        if (bits != 0) {
+          const int f = (int)((fidx >> (4 * u)) & 15u);
+          const int i = 16 * u + f;
+          const int j = base + __popcll(m & ((1ull << i) - 1ull));     // rank among the lane's survivors
+          if (j < seg_cap) dst[j] = make_key(fv[u], (uint32_t)(hl + 32 * u + 8 * (f >> 2) + (f & 3)));
+          rest |= (uint64_t)(bits & (bits - 1u)) << (16 * u);
+        }
+      }
+      if (!__any(rest != 0)) return;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t bits = (uint32_t)(rest >> (16 * u)) & 0xffffu;
+        if (!__any(bits != 0)) continue;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          *reinterpret_cast<float4*>(row + 4 * c) =
+              make_float4(acc[u][t][4 * c], acc[u][t][4 * c + 1], acc[u][t][4 * c + 2], acc[u][t][4 * c + 3]);
+        while (bits) {
+          const int v = __ffs(bits) - 1;
+          bits &= bits - 1;
+          const int i = 16 * u + v;
+          const int j = base + __popcll(m & ((1ull << i) - 1ull));
+          if (j < seg_cap) dst[j] = make_key(row[v], (uint32_t)(hl + 32 * u + 8 * (v >> 2) + (v & 3)));
+        }
+      }
+    };
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
 #pragma unroll
@@ -840,6 +891,8 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
       // For finite scores the sign of the rounded difference is exact: -0
       // only arises from a negative difference.
       uint32_t mk[4] = {0u, 0u, 0u, 0u};
+      float fv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      uint32_t fidx = 0;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         // The tile is copied out whole before use, so the 16 register reads
@@ -852,37 +905,43 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
         for (int v = 0; v < 16; ++v) sg[v] = __float_as_uint(thr[t] - tv[v]);
 #pragma unroll
         for (int v = 15; v >= 0; --v) mk[u] = __builtin_amdgcn_alignbit(mk[u], sg[v], 31);
-      }
-      const uint32_t lo = mk[0] | (mk[1] << 16), hi = mk[2] | (mk[3] << 16);
-      uint64_t m = ((uint64_t)hi << 32) | lo;
-      if (step_end - h0 < kStepRows) {                          // last, partial step
-        // r(i) grows with i, so the rows inside the step are the lowest
-        // bits: bits 4g..4g+3 are rows 8g..8g+3, hence the count below.
-        const int c = min(max(lim, 0), 128);
-        const int n_in = 4 * (c >> 3) + min(c & 7, 4);
-        m &= n_in >= 64 ? ~0ull : (1ull << n_in) - 1ull;
-      }
-      if (m == 0) continue;
-      const int ql = 128 * wq + 32 * t + l32;
-      const int base = atomicAdd(&cnt[ql], __popcll(m));
-      uint64_t* dst = seg + ((size_t)(q0 + ql) * n_chunks + chunk) * seg_cap;
-      int j = base;
+        mk[u] &= (uint32_t)(in_step >> (16 * u)) & 0xffffu;
+        if (__any(mk[u] != 0)) {
+          // Select tree on the bits of f, as bitwise selects under all-ones
+          // / all-zeros masks (one v_bfi each). The masks are opaque to the
+          // compiler, which would otherwise fold the tree into a dynamically
+          // indexed array and send it through memory.
+          const int f = (__ffs(mk[u]) - 1) & 15;
+          uint32_t sel[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        uint32_t bits = (uint32_t)(m >> (16 * u)) & 0xffffu;
-        if (bits == 0) continue;
+          for (int k = 0; k < 4; ++k) {
+            sel[k] = 0u - (uint32_t)((f >> k) & 1);
+            asm volatile("" : "+v"(sel[k]));
+          }
+          auto pick = [](uint32_t mask, uint32_t hi, uint32_t lo) { return (hi & mask) | (lo & ~mask); };
+          uint32_t a[8], b[4], c[2];
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          *reinterpret_cast<float4*>(row + 4 * c) =
-              make_float4(acc[u][t][4 * c], acc[u][t][4 * c + 1], acc[u][t][4 * c + 2], acc[u][t][4 * c + 3]);
-        while (bits) {
-          const int v = __ffs(bits) - 1;
-          bits &= bits - 1;
-          if (j < seg_cap) dst[j] = make_key(row[v], (uint32_t)(hl + 32 * u + 8 * (v >> 2) + (v & 3)));
-          ++j;
+          for (int v = 0; v < 8; ++v) a[v] = pick(sel[0], __float_as_uint(tv[2 * v + 1]), __float_as_uint(tv[2 * v]));
+#pragma unroll
+          for (int v = 0; v < 4; ++v) b[v] = pick(sel[1], a[2 * v + 1], a[2 * v]);
+#pragma unroll
+          for (int v = 0; v < 2; ++v) c[v] = pick(sel[2], b[2 * v + 1], b[2 * v]);
+          fv[u] = __uint_as_float(pick(sel[3], c[1], c[0]));
+          fidx |= (uint32_t)f << (4 * u);
         }
       }
+      const uint32_t lo = mk[0] | (mk[1] << 16), hi = mk[2] | (mk[3] << 16);
+      const uint64_t m = ((uint64_t)hi << 32) | lo;
+      const int ql = 128 * wq + 32 * t + l32;
+      const int base = m != 0 ? atomicAdd(&cnt[ql], __popcll(m)) : 0;
+      if (t > 0 && __any(m_prev != 0)) write_column(t - 1, m_prev, base_prev, f_prev, fv_prev);
+      m_prev = m;
+      base_prev = base;
+      f_prev = fidx;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) fv_prev[u] = fv[u];
     }
+    if (__any(m_prev != 0)) write_column(3, m_prev, base_prev, f_prev, fv_prev);
   };
   const int n_steps = (h_end - h_begin + kStepRows - 1) / kStepRows;
   ring::sweep(hist, N, h_begin, kStepRows, n_steps, h_end, queries, Q, q0, d, lds, epi);

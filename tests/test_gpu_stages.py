@@ -144,6 +144,23 @@ def test_histogram_vs_oracle(k, B, tau):
     parity.check_hist(ids, sims, host(counts), host(mass), L, edges, tau)
 
 
+@pytest.mark.parametrize("k,B,tau", [(64, 256, 0.8), (256, 1024, 0.9), (100, 37, 0.5), (32, 128, 0.8)])
+def test_histogram_many_requests_per_wave(k, B, tau):
+    """More requests than resident waves: each wave bins several requests in
+    turn, with the next requests' lists and lengths in flight."""
+    rng = np.random.default_rng(k * 7 + B)
+    N, Q = 100000, 20011
+    edges, _ = workloads.log_bins(16384, B)
+    L = rng.integers(1, 16385, size=N).astype(np.int32)
+    ids = rng.integers(0, N, size=(Q, k)).astype(np.int32)
+    ids[:, 1] = ids[:, 0]                       # a repeated neighbour id is binned twice
+    sims = rng.uniform(0.5, 1.0, size=(Q, k)).astype(np.float32)
+    ids[::97, k // 3:] = -1                     # some short lists
+    sims[::89] = 0.3                            # some rows below tau
+    counts, mass = sage.histogram(dev(ids), dev(sims), dev(L), tau, dev(edges))
+    parity.check_hist(ids, sims, host(counts), host(mass), L, edges, tau)
+
+
 # ------------------------------------------------------- index refresh (attained service)
 def test_index_attained_vs_oracle_full_index_workload():
     w = workloads.make_config(4)
