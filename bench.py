@@ -1,6 +1,6 @@
 """Benchmark of the scheduling-decision path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
 
 A step is one scheduling decision for a batch of pending requests: bf16
 ingest of the query embeddings, similarity search + top-k + histogram
@@ -34,9 +34,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4", "5", "ttlt"],
-                    help="workload: 1 tiny, 2 mid (default), 3 gemm-bound, 4 index-bound, 5 streaming, "
-                         "ttlt (a Poisson request trace replayed under FCFS / Mean / Gittins)")
+    ap.add_argument("--config", default="3", choices=["1", "2", "3", "4", "5", "ttlt"],
+                    help="workload: 1 tiny, 2 mid, 3 gemm-bound (default: the largest batch), 4 index-bound, "
+                         "5 streaming, ttlt (a Poisson request trace replayed under FCFS / Mean / Gittins)")
     ap.add_argument("--nodes", type=int, default=64, help="ttlt: servers (8 requests/s each)")
     ap.add_argument("--requests", type=int, default=32768, help="ttlt: requests in the trace")
     ap.add_argument("--load", type=float, default=0.9, help="ttlt: offered load per server")
@@ -74,14 +74,19 @@ def read_traffic(kernel: str, workload_key: str, sources=("k_sim_topk.hip", "sag
         return None
 
 
-def stage_rooflines(stages, rows_per_launch: float, d: int, k: int, B: int):
+def stage_rooflines(stages, rows_per_launch: float, d: int, k: int, B: int, search=None):
     """The HBM-bound stages of the decision: algorithmic bytes per launch
     (query ingest 6 B per element; histogram Q(12k + 8B): ids, sims and the
     gathered lengths in, counts and masses out; index Q(4B + 8): masses and
-    prompt lengths in, index out) over the mean launch time from the timer."""
+    prompt lengths in, index out; candidate select: 8 B per candidate key and
+    4 B per segment count in, a flag and k ids + sims per query out, the key
+    count from sage_predict_stats) over the mean launch time from the timer."""
     per = {"ingest_bf16": 6.0 * rows_per_launch * d,
            "hist": rows_per_launch * (12.0 * k + 8.0 * B),
            "index_scan": rows_per_launch * (4.0 * B + 8.0)}
+    if search is not None:
+        per["topk_select"] = (8.0 * search["candidate_keys"] + 4.0 * rows_per_launch * search["segments_per_query"]
+                              + rows_per_launch * (4.0 + 8.0 * k))
     out = {}
     for name, byts in per.items():
         if name not in stages:
@@ -102,12 +107,17 @@ def kernel_name(k: int, Q: int = 1 << 30) -> str:
     return "sim_filter_kernel" if k <= 64 else "sim_topk_kernel"
 
 
+def oracle_threads() -> int:
+    return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle (as it stands) on a bounded sample of the same batch."""
     import oracle
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = oracle_threads()
     spec = w.spec
-    hb = oracle.round_to_bf16(w.hist_emb)          # the resident store: not timed, as on the GPU
+    # the resident store, rounded and widened once: not timed, as on the GPU
+    hb = oracle.bf16_to_f64(oracle.round_to_bf16(w.hist_emb))
     block = 128
     done = 0
     t_total = 0.0
@@ -123,6 +133,53 @@ def cpu_baseline(w, budget_s: float):
     return {"value": done / t_total, "unit": "decisions/s", "cores": threads, "kind": "oracle",
             "sample": f"first {done} of the {spec.Q} requests of one batch (full history), "
                       f"{t_total:.1f} s of CPU time; ranking within the sample"}
+
+
+def cpu_baseline_index(w, budget_s: float):
+    """The oracle's cost + Gittins index + rank on blocks of the index-bound
+    batch until about budget_s of CPU time."""
+    import oracle
+    spec = w.spec
+    block = 4096
+    done, t_total = 0, 0.0
+    while done < spec.Q and t_total < budget_s:
+        rows = slice(done, min(spec.Q, done + block))
+        t0 = time.perf_counter()
+        oracle.schedule(w.mass[rows], w.prompt_len[rows], w.bin_repr)
+        t_total += time.perf_counter() - t0
+        done = rows.stop
+    return {"value": done / t_total, "unit": "decisions/s", "cores": oracle_threads(), "kind": "oracle",
+            "sample": f"first {done} of the {spec.Q} requests ({spec.B} bins each), blocks of {block}, "
+                      f"{t_total:.1f} s of CPU time; ranking within each block"}
+
+
+def cpu_baseline_streaming(w, standing: int, batch: int, budget_s: float):
+    """The oracle's work per streaming decision on the first calls: search +
+    histogram of the call's arrivals against the whole store, then cost +
+    Gittins index + rank of a standing queue of standing + batch rows, until
+    about budget_s of CPU time."""
+    import oracle
+    spec = w.spec
+    hb = oracle.bf16_to_f64(oracle.round_to_bf16(w.hist_emb))     # resident store, untimed
+    threads = oracle_threads()
+    n_calls = spec.Q // batch
+    calls, t_total = 0, 0.0
+    plen_queue = np.resize(w.prompt_len, standing + batch)
+    while calls < n_calls and t_total < budget_s:
+        a = calls * batch
+        t0 = time.perf_counter()
+        qb = oracle.round_to_bf16(w.queries[a:a + batch])
+        ids, sims = oracle.search(qb, hb, spec.k, block=batch, threads=threads)
+        _, mass = oracle.histogram(ids, sims, w.hist_len, w.bin_edges, spec.tau)
+        queue_mass = np.resize(mass, (standing + batch, spec.B))
+        oracle.schedule(queue_mass, plen_queue, w.bin_repr)
+        t_total += time.perf_counter() - t0
+        calls += 1
+    return {"value": calls * batch / t_total, "unit": "decisions/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {calls} of the {n_calls} decisions: each searches its {batch} arrivals against "
+                      f"all {spec.N} rows, then costs, indexes and ranks a queue of {standing + batch} rows "
+                      f"(masses: the call's own predictions repeated, values do not change the work); "
+                      f"{t_total:.1f} s of CPU time"}
 
 
 def main():
@@ -205,6 +262,7 @@ def main():
     stages = timer.totals()
     timer.close()
     print(f"# step: {1e3 * elapsed / args.steps:.3f} ms", file=sys.stderr, flush=True)
+    search = sage.predict_stats(ws, Q, N, d, k, B)      # the last (timed) step's search; synchronises
 
     ms_per_step = 1e3 * elapsed / args.steps
     value = Q * args.steps / elapsed
@@ -235,7 +293,8 @@ def main():
                      "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
                      "avg_launch_us": k1_avg_s * 1e6, "flops_per_launch": flops},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
-        "stage_rooflines": stage_rooflines(stages, Q, d, k, B),
+        "stage_rooflines": stage_rooflines(stages, Q, d, k, B, search),
+        "search": search,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
@@ -316,6 +375,8 @@ def run_index_bound(args, torch, sage, workloads):
                              "achieved_GBs": att_bytes / att_s / 1e9,
                              "frac_of_hbm_peak": att_bytes / att_s / 1e9 / HBM_PEAK_GBS},
     }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_index(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 
@@ -334,7 +395,6 @@ def run_streaming(args, torch, sage, workloads):
     log("ingesting the store")
     store = sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr), spec.k,
                        spec.tau)
-    del w.hist_emb
     torch.cuda.empty_cache()
     log("predicting the standing queue")
     _, _, _, smass = store.predict(dev(sq))
@@ -394,6 +454,9 @@ def run_streaming(args, torch, sage, workloads):
                                              sources=("k_sim_stream.hip", "sage_device.hpp")), "avg_launch_us": k1_avg_s * 1e6, "bytes_per_launch": k1_bytes},
         "stages_us_per_step": {name: 1e3 * ms / args.steps for name, (n, ms) in stages.items()},
     }
+    if not args.no_cpu_baseline:
+        log("cpu baseline")
+        line["cpu_baseline"] = cpu_baseline_streaming(w, standing, batch, args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 

@@ -187,6 +187,26 @@ int sage_predict_layout(const uint16_t* queries, int query_layout, int Q,
                         void* workspace, size_t workspace_bytes, sage_stream_t stream);
 
 /*
+ * sage_predict_stats - what the last sage_predict / sage_predict_layout call
+ * with this workspace and these sizes did in its neighbour search, for
+ * measurement (the candidate keys are the select stage's input; their count
+ * depends on the data). Copies a few counters from the workspace to the host
+ * and SYNCHRONISES `stream`: not for the decision path itself.
+ *   stats [5] host, out:
+ *     [0] search path: 0 exact per-chunk lists, 1 filtered (k <= 64),
+ *         2 few-query stream search
+ *     [1] candidate keys written for the select stage (list path: every
+ *         list entry, Q * [3] * [4])
+ *     [2] queries sent to the exact fallback
+ *     [3] candidate segments (lists) per query
+ *     [4] capacity of a segment (list length)
+ * SAGE_EINVAL for sizes as in sage_predict or stats NULL; SAGE_EWORKSPACE
+ * when the workspace is smaller than that call needs.
+ */
+int sage_predict_stats(const void* workspace, size_t workspace_bytes, int Q, int N, int d, int k, int B,
+                       long long* stats, sage_stream_t stream);
+
+/*
  * sage_predict_noalloc - sage_predict_layout for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc): the same search with no workspace

@@ -125,10 +125,11 @@ def search(q_bits, h_bits, k: int, block: int = 128, threads: int | None = None)
     """Similarity + top-k over the whole store, one query block at a time.
 
     Blocking over queries only bounds memory; each row is still the plain
-    definition (full fp64 score row, then ``topk_row``).
+    definition (full fp64 score row, then ``topk_row``). The store may be
+    given already widened to fp64 (``bf16_to_f64``).
     """
     Q = q_bits.shape[0]
-    hf = bf16_to_f64(h_bits)
+    hf = h_bits if np.asarray(h_bits).dtype == np.float64 else bf16_to_f64(h_bits)
     ids = np.empty((Q, k), dtype=np.int32)
     sims = np.empty((Q, k), dtype=np.float64)
     threads = threads or os.cpu_count() or 1

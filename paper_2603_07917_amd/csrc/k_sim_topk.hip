@@ -417,17 +417,6 @@ __device__ __forceinline__ uint64_t fold_group(uint64_t list, uint64_t key) {
   return wave_bitonic_clean_desc64(list > asc ? list : asc);
 }
 
-// Wave 0 folds the lists of waves 1..3 (in LDS) into its own.
-__device__ __forceinline__ uint64_t fold_lists(uint64_t list, const uint64_t (&lists)[4][kWave]) {
-  const int lane = (int)lane_id();
-#pragma unroll
-  for (int o = 1; o < 4; ++o) {
-    const uint64_t other = lists[o][kWave - 1 - lane];
-    list = wave_bitonic_clean_desc64(list > other ? list : other);
-  }
-  return list;
-}
-
 // theta0: the k-th largest of a query's m (<= 512 * 16) group maxima, held
 // in registers as monotone key bits (VPL per lane; past m: key 0, below every
 // real score). theta0 is the largest key T with at least k keys >= T, built
@@ -949,55 +938,50 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
   if (q0 + tid < Q) seg_count[(size_t)(q0 + tid) * n_chunks + chunk] = cnt[tid];
 }
 
-// Select kernel: one workgroup (4 waves) per query. Wave w reads the query's
-// segments w, w + 4, ... straight from global memory, 64 keys at a time. Each
-// wave keeps its best 64 keys as a descending list across lanes; keys that
+// Select kernel: one wavefront per query, four queries per workgroup. The
+// wave reads the query's candidate keys straight from global memory (its
+// segments form one index range; kPre groups of 64 keys in flight at once)
+// and keeps its best 64 keys as a descending list across lanes: keys that
 // beat the list's last key are gathered in LDS, and each 64 of them are
 // sorted (wave bitonic sort) and folded in with C_i = max(A_i, B_{63-i}) and
-// six half-cleaner stages. Wave 0 then folds in
-// the other three lists and writes the first k. A query with an overflowed
-// segment, or with fewer than min(k, N) candidates in all, is flagged for
-// the exact fallback and left untouched here.
+// six half-cleaner stages. One list per query means only the keys that beat
+// the query's running 64th are sorted (about k (1 + ln(n / k)) of n), not
+// those of four partial lists. A query with an overflowed segment, or with
+// fewer than min(k, N) candidates in all, is flagged for the exact fallback
+// and left untouched here. Waves work independently (no workgroup barrier).
 __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict__ seg,
-                                                     const int* __restrict__ seg_count, int n_chunks,
+                                                     const int* __restrict__ seg_count, int Q, int n_chunks,
                                                      int seg_cap, int k, int need, int* __restrict__ flags,
                                                      int32_t* __restrict__ ids, float* __restrict__ sims) {
-  __shared__ int off[kWave + 1];
-  __shared__ int over;
-  __shared__ uint64_t lists[4][kWave];
+  __shared__ int off_s[4][kWave + 1];
   __shared__ uint64_t pend[4][2 * kWave];
-  const int q = blockIdx.x;
-  const int tid = threadIdx.x;
   const int lane = (int)lane_id();
-  const int w = tid / kWave;
-  if (w == 0) {                                       // n_chunks <= 64: one segment per lane
-    const int n = lane < n_chunks ? seg_count[(size_t)q * n_chunks + lane] : 0;
-    const int c = min(n, seg_cap);
-    int incl = c;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int q = blockIdx.x * 4 + w;
+  if (q >= Q) return;
+  int* off = off_s[w];
+  // Segment c (one per lane; n_chunks <= 64) starts at off[c] of the range.
+  const int n = lane < n_chunks ? seg_count[(size_t)q * n_chunks + lane] : 0;
+  const int c = min(n, seg_cap);
+  int incl = c;
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int y = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += y;
-    }
-    off[lane] = incl - c;
-    if (lane == kWave - 1) off[kWave] = incl;
-    // Flag the query when a segment overflowed, or when fewer than
-    // min(k, N) keys beat theta0: the pre-pass scores are the filter's own,
-    // bit for bit, so the latter only follows from a raised threshold.
-    const bool ov = __any(n > seg_cap) || __shfl(incl, kWave - 1, kWave) < need;
-    if (lane == 0) over = ov ? 1 : 0;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
   }
-  __syncthreads();
-  if (over) {
-    if (tid == 0) flags[q] = 1;
+  off[lane] = incl - c;
+  if (lane == kWave - 1) off[kWave] = incl;
+  const int total = __shfl(incl, kWave - 1, kWave);
+  // Flag the query when a segment overflowed, or when fewer than min(k, N)
+  // keys beat theta0: the pre-pass scores are the filter's own, bit for
+  // bit, so the latter only follows from a raised threshold.
+  if (__any(n > seg_cap) || total < need) {
+    if (lane == 0) flags[q] = 1;
     return;
   }
-  if (tid == 0) flags[q] = 0;
+  if (lane == 0) flags[q] = 0;
+  __builtin_amdgcn_wave_barrier();                    // off[] written before it is read
   const uint64_t* src = seg + (size_t)q * n_chunks * seg_cap;
-  // Keys that beat the list's current last key are packed into a per-wave
-  // LDS buffer (ballot positions); a sort-and-merge runs once 64 have
-  // gathered, instead of once per group that holds any of them. Wave w
-  // reads segments w, w + 4, ..., 64 consecutive keys at a time.
   uint64_t* buf = pend[w];
   uint64_t list = kPadKey;
   int n_buf = 0;                                      // keys waiting in buf (wave-uniform, < 64)
@@ -1020,42 +1004,26 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
       __builtin_amdgcn_wave_barrier();
     }
   };
-  // The first 64 keys of kPre segments are loaded at once (segments hold
-  // about a thousand keys / n_chunks, mostly fewer than 64), then consumed
-  // in order; longer segments finish with further loads.
   constexpr int kPre = 8;
-  for (int cb = w; cb < n_chunks; cb += 4 * kPre) {
+  for (int e0 = 0; e0 < total; e0 += kWave * kPre) {
     uint64_t cur[kPre];
-    int n_c[kPre];
 #pragma unroll
     for (int j = 0; j < kPre; ++j) {
-      const int c = cb + 4 * j;
-      n_c[j] = c < n_chunks ? off[c + 1] - off[c] : 0;
-      cur[j] = lane < n_c[j] ? src[(size_t)c * seg_cap + lane] : kPadKey;
+      const int e = e0 + kWave * j + lane;
+      cur[j] = kPadKey;
+      if (e < total) {
+        int lo = 0, hi = n_chunks - 1;                // the last segment c with off[c] <= e
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (off[mid] <= e) lo = mid; else hi = mid - 1;
+        }
+        cur[j] = src[(size_t)lo * seg_cap + (e - off[lo])];
+      }
     }
-    // One copy of the consuming code: the registers shift down each turn.
-#pragma unroll 1
-    for (int j = 0; j < kPre; ++j) {
-      uint64_t x = cur[0];
-      const int nx = n_c[0];
 #pragma unroll
-      for (int i = 0; i + 1 < kPre; ++i) {
-        cur[i] = cur[i + 1];
-        n_c[i] = n_c[i + 1];
-      }
-      const uint64_t* sp = src + (size_t)(cb + 4 * j) * seg_cap;
-      for (int i0 = kWave;; i0 += kWave) {
-        take(x);
-        if (i0 >= nx) break;
-        x = i0 + lane < nx ? sp[i0 + lane] : kPadKey;
-      }
-    }
+    for (int j = 0; j < kPre; ++j) take(cur[j]);
   }
   if (n_buf > 0) list = fold_group(list, lane < n_buf ? buf[lane] : kPadKey);
-  lists[w][lane] = list;
-  __syncthreads();
-  if (w != 0) return;
-  list = fold_lists(list, lists);
   if (lane < k) {
     ids[(size_t)q * k + lane] = list == kPadKey ? -1 : key_id(list);
     sims[(size_t)q * k + lane] = list == kPadKey ? -__builtin_inff() : key_sim(list);
@@ -1253,7 +1221,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     }
     {
       LaunchScope scope("topk_select", stream);
-      hipLaunchKernelGGL(select_kernel, dim3(Q), dim3(256), 0, stream, seg, segcnt,
+      hipLaunchKernelGGL(select_kernel, dim3((Q + 3) / 4), dim3(256), 0, stream, seg, segcnt, Q,
                          p.f_n_chunks, p.seg_cap, k, min(k, N), flags, ids, sims);
     }
     // Exact fallback for queries whose candidates overflowed (no work otherwise).

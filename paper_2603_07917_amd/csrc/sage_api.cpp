@@ -410,6 +410,55 @@ SAGE_API int sage_predict_noalloc(const uint16_t* queries, int query_layout, int
                              nbr_ids, nbr_sims, counts, mass, ws, (size_t)SAGE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
+SAGE_API int sage_predict_stats(const void* workspace, size_t workspace_bytes, int Q, int N, int d, int k, int B,
+                               long long* stats, sage_stream_t stream) {
+  int st = check_predict_sizes(Q, N, d, k, B);
+  if (st != SAGE_OK) return st;
+  if (!stats) return fail(SAGE_EINVAL, "sage_predict_stats: stats is NULL");
+  for (int i = 0; i < 5; ++i) stats[i] = 0;
+  if (Q == 0) return ok();
+  const sage::SimTopkPlan plan = sage::plan_sim_topk(Q, N, d, k);
+  if (!workspace || workspace_bytes < plan.workspace_bytes())
+    return fail(SAGE_EWORKSPACE, "sage_predict_stats: workspace of %zu bytes, %zu needed", workspace_bytes,
+                plan.workspace_bytes());
+  if ((st = check_device()) != SAGE_OK) return st;
+  const char* ws = static_cast<const char*>(workspace);
+  hipStream_t s = (hipStream_t)stream;
+  std::vector<int32_t> counts, flags;
+  int per_query = 0, cap = 0;
+  if (plan.fast) {
+    stats[0] = 1;
+    per_query = plan.f_n_chunks;
+    cap = plan.seg_cap;
+  } else if (plan.stream) {
+    stats[0] = 2;
+    per_query = 1;
+    cap = plan.s_cap;
+  } else {
+    stats[0] = 0;
+    stats[1] = (long long)Q * plan.n_chunks * plan.list_len;
+    stats[3] = plan.n_chunks;
+    stats[4] = plan.list_len;
+    return ok();
+  }
+  counts.resize((size_t)Q * per_query);
+  flags.resize(Q);
+  hipError_t e = hipMemcpyAsync(counts.data(), ws + (plan.fast ? plan.off_segcnt : plan.off_ccount),
+                                counts.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(flags.data(), ws + plan.off_flags, flags.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_status(e, "sage_predict_stats copy");
+  long long keys = 0, flagged = 0;
+  for (int32_t c : counts) keys += c < cap ? c : cap;
+  for (int32_t f : flags) flagged += f != 0;
+  stats[1] = keys;
+  stats[2] = flagged;
+  stats[3] = per_query;
+  stats[4] = cap;
+  return ok();
+}
+
 SAGE_API int sage_predict(const uint16_t* queries, int Q, const uint16_t* hist_emb,
                           const int32_t* hist_len, int N, int d, int k, float tau,
                           const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims,

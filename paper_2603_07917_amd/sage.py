@@ -57,6 +57,7 @@ def load_library():
         "sage_mix_uniform": (I, [P, I, I, F, P, S]),
         "sage_check_inputs": (I, [P, P, I, P, I, P, S]),
         "sage_predict_noalloc": (I, [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, S]),
+        "sage_predict_stats": (I, [P, Z, I, I, I, I, I, ctypes.POINTER(ctypes.c_longlong), S]),
         "sage_debug_theta_floor": (I, [F]),
         "sage_status_string": (ctypes.c_char_p, [I]),
         "sage_last_error": (ctypes.c_char_p, []),
@@ -366,6 +367,17 @@ def simulate(arrival, prompt_len, output_len, order, *, rate: float, servers: in
                                         int(levels), n_inf, int(bucket), int(servers), float(rate),
                                         int(queue_cap), finish.ctypes.data, pre.ctypes.data))
     return finish, pre
+
+
+def predict_stats(workspace: torch.Tensor, Q: int, N: int, d: int, k: int, B: int) -> dict:
+    """What the last predict with this workspace did (sage_predict_stats;
+    synchronises the current stream)."""
+    out = (ctypes.c_longlong * 5)()
+    _check(load_library().sage_predict_stats(workspace.data_ptr(), workspace.numel(), Q, N, d, k, B, out,
+                                             _stream()))
+    path = {0: "lists", 1: "filtered", 2: "stream"}[int(out[0])]
+    return {"path": path, "candidate_keys": int(out[1]), "flagged": int(out[2]),
+            "segments_per_query": int(out[3]), "segment_capacity": int(out[4])}
 
 
 CHECK_BITS = {1: "bin edges not finite and strictly increasing",
