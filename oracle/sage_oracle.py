@@ -23,6 +23,8 @@ Stages and the passages they follow:
   G(D) = inf_{Delta>0} E[min(X, Delta)] / P(X <= Delta), X ~ D.
 * ``rank``            - Sec. 3.3: the smaller index is served first; ties go
   to the lower request id.
+* ``length_similarity`` / ``predict_by_length`` - Sec. 4.3's semantic-unaware
+  predictor: neighbours by similar input length instead of similar prompt.
 
 Every function here is pinned by ``-m "not gpu"`` tests against brute force,
 exact rational arithmetic, closed forms and invariants (tests/test_oracle_*.py).
@@ -141,6 +143,23 @@ def search(q_bits, h_bits, k: int, block: int = 128, threads: int | None = None)
             for r, (i, v) in enumerate(rows):
                 ids[s0 + r], sims[s0 + r] = i, v
     return ids, sims
+
+
+def length_similarity(prompt_len, hist_prompt_len, max_len: int) -> np.ndarray:
+    """Input-length similarity of the semantic-unaware predictor (Sec. 4.3's
+    predictor ablation: history records with a similar input length stand in
+    for similar prompts). Reading: s(I, L) = min(I, L) / max(I, L), the
+    ratio of the shorter to the longer prompt, in (0, 1] and 1 for equal
+    lengths, so that the predictor's similarity threshold (0.8) keeps its
+    meaning (within a factor 1.25). It is defined as the fp32 quotient of the
+    two lengths (correctly rounded), the precision in which the neighbour
+    choice is made. Lengths below 1 count as 1, history lengths above
+    max_len as max_len. Returns [Q, N] fp32 values widened to fp64."""
+    I = np.maximum(np.asarray(prompt_len, dtype=np.int64), 1)[:, None]
+    L = np.clip(np.asarray(hist_prompt_len, dtype=np.int64), 1, int(max_len))[None, :]
+    a = np.minimum(I, L).astype(np.float32)
+    b = np.maximum(I, L).astype(np.float32)
+    return (a / b).astype(np.float64)
 
 
 # -------------------------------------------------------------- histogram
@@ -315,6 +334,17 @@ def predict(queries_f32, hist_f32, hist_len, k, tau, edges, *, block=128, thread
     qb = round_to_bf16(queries_f32)
     hb = round_to_bf16(hist_f32)
     ids, sims = search(qb, hb, k, block=block, threads=threads)
+    counts, mass = histogram(ids, sims, hist_len, edges, tau)
+    return ids, sims, counts, mass
+
+
+def predict_by_length(prompt_len, hist_prompt_len, max_len, hist_len, k, tau, edges):
+    """The semantic-unaware history-based predictor (Sec. 4.3): the k history
+    records with the most similar input length (``length_similarity``, ties
+    to the lower index), then the same similarity-weighted histogram as the
+    semantic predictor ("the same filtering method")."""
+    S = length_similarity(prompt_len, hist_prompt_len, max_len)
+    ids, sims = topk(S, k)
     counts, mass = histogram(ids, sims, hist_len, edges, tau)
     return ids, sims, counts, mass
 

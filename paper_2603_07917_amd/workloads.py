@@ -37,7 +37,8 @@ import numpy as np
 SEED_BASE = 260307917
 # Order in which child streams are spawned; never reorder (changes every input).
 STREAMS = ("centres", "cluster_params", "assignment", "noise", "lengths",
-           "queries", "prompt_lengths", "masses", "standing", "attained", "trace")
+           "queries", "prompt_lengths", "masses", "standing", "attained", "trace",
+           "hist_prompt_lengths")
 
 
 def streams(config_id: int, seed_base: int = SEED_BASE) -> dict:
@@ -148,6 +149,7 @@ class PredictInputs:
     bin_edges: np.ndarray     # [B+1] float64
     bin_repr: np.ndarray      # [B] float64
     seed: list
+    hist_prompt_len: Optional[np.ndarray] = None   # [N] int32: input lengths of the stored records
 
 
 def _cluster_probs(spec: PredictSpec, rng) -> np.ndarray:
@@ -215,9 +217,13 @@ def make_predict(spec: PredictSpec, config_id: int, seed_base: int = SEED_BASE) 
     queries = _points(rq, centres, q_cluster, spec, q_noise)
 
     prompt_len = _prompt_lengths(r["prompt_lengths"], spec.prompt, spec.Q)
+    # Input lengths of the stored records, from the same law as the pending
+    # requests' and independent of everything else (the stand-in data carry
+    # no relation between input and output length).
+    hist_prompt_len = _prompt_lengths(r["hist_prompt_lengths"], spec.prompt, spec.N)
     edges, repr_ = log_bins(spec.L_max, spec.B)
     return PredictInputs(spec, hist_emb, hist_len, hist_cluster, queries, q_cluster,
-                         prompt_len, edges, repr_, [seed_base, config_id])
+                         prompt_len, edges, repr_, [seed_base, config_id], hist_prompt_len)
 
 
 @dataclass
