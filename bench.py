@@ -538,6 +538,20 @@ def run_ttlt(args, torch, sage, workloads):
         o, lv, inf_n = simulator.policy_order(pol, mass, plen, store.bin_repr, tr.arrival, tr.output_len,
                                               bucket, noise=0.2)
         host_orders[pol + "+noise"] = (o.cpu().numpy(), lv, inf_n, pol == "gittins")
+    # The same policies on the semantic-unaware predictor (Sec. 4.3: the
+    # history records with the most similar input length), outside the timed
+    # region. The stand-in data carry no relation between input and output
+    # length, so its distributions are close to the store's overall one.
+    len_index = sage.LengthIndex(dev(w.hist_prompt_len), spec.L_max)
+    mass_len = torch.empty_like(mass)
+    for s in range(0, R, chunk):
+        e = min(R, s + chunk)
+        sage.predict_by_length(plen[s:e], len_index, store.hist_len, spec.k, spec.tau, store.bin_edges,
+                               out=tuple(t[:e - s] for t in pred_out) + (mass_len[s:e],))
+    for pol in ("mean", "gittins-static", "gittins"):
+        o, lv, inf_n = simulator.policy_order(pol, mass_len, plen, store.bin_repr, tr.arrival, tr.output_len,
+                                              bucket)
+        host_orders[pol + "+length"] = (o.cpu().numpy(), lv, inf_n, pol == "gittins")
 
     def replay(arrival, servers, rate_s):
         out = {}

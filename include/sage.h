@@ -187,6 +187,47 @@ int sage_predict_layout(const uint16_t* queries, int query_layout, int Q,
                         void* workspace, size_t workspace_bytes, sage_stream_t stream);
 
 /*
+ * sage_length_index - the store's records ordered by input length, for the
+ * semantic-unaware predictor below (Sec. 4.3's predictor ablation). Build it
+ * once per store (and again after records change).
+ *   hist_prompt_len [N] int32  input lengths of the stored records, clamped
+ *                              to [1, max_len]
+ *   max_len                    1..2^20
+ *   by_len [N] int32 out       record indices sorted by clamped length, equal
+ *                              lengths by ascending index
+ *   sorted_len [N] int32 out   their clamped lengths
+ *   len_off [max_len + 2] int32 out  len_off[L] = first position in by_len
+ *                              whose length is >= L (N if none)
+ *   workspace                  >= sage_length_index_workspace_bytes(N) bytes
+ * SAGE_EINVAL: N < 1, max_len outside [1, 2^20], NULL or misaligned pointers;
+ * SAGE_EWORKSPACE: workspace too small.
+ */
+size_t sage_length_index_workspace_bytes(int N);
+int sage_length_index(const int32_t* hist_prompt_len, int N, int max_len, int32_t* by_len, int32_t* sorted_len,
+                      int32_t* len_off, void* workspace, size_t workspace_bytes, sage_stream_t stream);
+
+/*
+ * sage_predict_by_length - the semantic-unaware history-based predictor
+ * (Sec. 4.3): neighbours are the stored records with the most similar INPUT
+ * LENGTH rather than the most similar prompt. The similarity of input
+ * lengths I and L is s = min(I, L) / max(I, L) (fp32, correctly rounded;
+ * I below 1 counts as 1), so the threshold tau keeps its meaning for the
+ * predictor ("the same filtering method"). The k records with the largest s
+ * (ties to the lower index; padding -1 / -inf when N < k) then go through
+ * the histogram of sage_predict: counts and s-weighted masses with tau.
+ *   prompt_len [Q] int32       input lengths of the pending requests
+ *   by_len, sorted_len, len_off, max_len   the index from sage_length_index
+ *   hist_len [N] int32         recorded output lengths of the stored records
+ *   other arguments and outputs as in sage_predict (nbr_sims holds s).
+ * Q = 0 is a no-op. SAGE_EINVAL for sizes as in sage_predict, max_len outside
+ * [1, 2^20], NULL or misaligned pointers.
+ */
+int sage_predict_by_length(const int32_t* prompt_len, int Q, const int32_t* by_len, const int32_t* sorted_len,
+                           const int32_t* len_off, int max_len, const int32_t* hist_len, int N, int k, float tau,
+                           const double* bin_edges, int B, int32_t* nbr_ids, float* nbr_sims, int32_t* counts,
+                           float* mass, sage_stream_t stream);
+
+/*
  * sage_predict_stats - what the last sage_predict / sage_predict_layout call
  * with this workspace and these sizes did in its neighbour search, for
  * measurement (the candidate keys are the select stage's input; their count

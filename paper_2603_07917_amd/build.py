@@ -21,7 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsage.so")
 
 SOURCES = ["sage_api.cpp", "sim.cpp", "k_elementwise.hip", "k_index_rank.hip", "k_hist.hip",
-           "k_topk_merge.hip", "k_sim_topk.hip", "k_sim_stream.hip"]
+           "k_topk_merge.hip", "k_sim_topk.hip", "k_sim_stream.hip", "k_length.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

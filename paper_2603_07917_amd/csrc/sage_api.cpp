@@ -507,6 +507,63 @@ SAGE_API int sage_histogram_variant(const int32_t* nbr_ids, const float* nbr_sim
                         stream);
 }
 
+// ------------------------------------------ predict by input length
+SAGE_API size_t sage_length_index_workspace_bytes(int N) {
+  return N > 0 ? sage::length_index_workspace_bytes(N) : 0;
+}
+
+SAGE_API int sage_length_index(const int32_t* hist_prompt_len, int N, int max_len, int32_t* by_len,
+                               int32_t* sorted_len, int32_t* len_off, void* workspace, size_t workspace_bytes,
+                               sage_stream_t stream) {
+  if (N < 1) return fail(SAGE_EINVAL, "N=%d must be >= 1", N);
+  if (max_len < 1 || max_len > sage::kLengthMaxLen)
+    return fail(SAGE_EINVAL, "max_len=%d outside [1, %d]", max_len, sage::kLengthMaxLen);
+  const void* ptrs[] = {hist_prompt_len, by_len, sorted_len, len_off};
+  for (const void* p : ptrs) {
+    if (!p) return fail(SAGE_EINVAL, "sage_length_index: NULL pointer");
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_length_index: misaligned pointer");
+  }
+  const size_t need = sage::length_index_workspace_bytes(N);
+  if (!workspace || workspace_bytes < need)
+    return fail(SAGE_EWORKSPACE, "sage_length_index: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(SAGE_EINVAL, "sage_length_index: workspace is not 16-byte aligned");
+  int st = check_device();
+  if (st != SAGE_OK) return st;
+  return hip_status(sage::launch_length_index(hist_prompt_len, N, max_len, by_len, sorted_len, len_off, workspace,
+                                              (hipStream_t)stream),
+                    "length index launch");
+}
+
+SAGE_API int sage_predict_by_length(const int32_t* prompt_len, int Q, const int32_t* by_len,
+                                    const int32_t* sorted_len, const int32_t* len_off, int max_len,
+                                    const int32_t* hist_len, int N, int k, float tau, const double* bin_edges, int B,
+                                    int32_t* nbr_ids, float* nbr_sims, int32_t* counts, float* mass,
+                                    sage_stream_t stream) {
+  if (Q < 0) return fail(SAGE_EINVAL, "Q=%d is negative", Q);
+  if (N < 1) return fail(SAGE_EINVAL, "N=%d must be >= 1", N);
+  if (k < 1 || k > SAGE_MAX_K) return fail(SAGE_EINVAL, "k=%d outside [1, %d]", k, SAGE_MAX_K);
+  if (B < 1 || B > SAGE_MAX_BINS) return fail(SAGE_EINVAL, "B=%d outside [1, %d]", B, SAGE_MAX_BINS);
+  if (max_len < 1 || max_len > sage::kLengthMaxLen)
+    return fail(SAGE_EINVAL, "max_len=%d outside [1, %d]", max_len, sage::kLengthMaxLen);
+  int st = check_tau(tau);
+  if (st != SAGE_OK) return st;
+  if (Q == 0) return ok();
+  if ((st = check_bins(bin_edges, B)) != SAGE_OK) return st;
+  const void* ptrs[] = {prompt_len, by_len, sorted_len, len_off, hist_len, nbr_ids, nbr_sims, counts, mass};
+  for (const void* p : ptrs) {
+    if (!p) return fail(SAGE_EINVAL, "sage_predict_by_length: NULL pointer");
+    if (!aligned16(p)) return fail(SAGE_EINVAL, "sage_predict_by_length: misaligned pointer");
+  }
+  if ((st = check_device()) != SAGE_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = sage::launch_length_neighbours(prompt_len, Q, by_len, sorted_len, len_off, max_len, N, k, nbr_ids,
+                                                nbr_sims, s);
+  if (e != hipSuccess) return hip_status(e, "length neighbours launch");
+  e = sage::launch_hist(nbr_ids, nbr_sims, Q, k, hist_len, N, tau, bin_edges, B, SAGE_WEIGHT_SIMILARITY, counts,
+                        mass, s);
+  return hip_status(e, "hist launch");
+}
+
 // --------------------------------------------------------- cost / index
 SAGE_API int sage_cost(const int32_t* prompt_len, int Q, const double* bin_repr, int B, float* cost,
                        sage_stream_t stream) {

@@ -126,6 +126,16 @@ hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, cons
                        float* mass, hipStream_t stream);
 
 
+// Semantic-unaware predictor: the store's length index and the neighbours by
+// input-length similarity.
+constexpr int kLengthMaxLen = 1 << 20;
+size_t length_index_workspace_bytes(int N);
+hipError_t launch_length_index(const int32_t* hist_prompt_len, int N, int max_len, int32_t* by_len,
+                               int32_t* sorted_len, int32_t* off, void* ws, hipStream_t stream);
+hipError_t launch_length_neighbours(const int32_t* prompt_len, int Q, const int32_t* by_len,
+                                    const int32_t* sorted_len, const int32_t* off, int max_len, int N, int k,
+                                    int32_t* ids, float* sims, hipStream_t stream);
+
 // Host event loop of sage_simulate (inputs already validated); 0 on success.
 int simulate_queue(const double* arrival, const int32_t* prompt_len, const int32_t* output_len, int R,
                    const int32_t* order, int levels, int informed, int bucket, int servers,

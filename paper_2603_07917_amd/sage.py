@@ -58,6 +58,9 @@ def load_library():
         "sage_check_inputs": (I, [P, P, I, P, I, P, S]),
         "sage_predict_noalloc": (I, [P, I, I, P, I, P, I, I, I, F, P, I, P, P, P, P, S]),
         "sage_predict_stats": (I, [P, Z, I, I, I, I, I, ctypes.POINTER(ctypes.c_longlong), S]),
+        "sage_length_index_workspace_bytes": (Z, [I]),
+        "sage_length_index": (I, [P, I, I, P, P, P, P, Z, S]),
+        "sage_predict_by_length": (I, [P, I, P, P, P, I, P, I, I, F, P, I, P, P, P, P, S]),
         "sage_debug_theta_floor": (I, [F]),
         "sage_status_string": (ctypes.c_char_p, [I]),
         "sage_last_error": (ctypes.c_char_p, []),
@@ -378,6 +381,50 @@ def predict_stats(workspace: torch.Tensor, Q: int, N: int, d: int, k: int, B: in
     path = {0: "lists", 1: "filtered", 2: "stream"}[int(out[0])]
     return {"path": path, "candidate_keys": int(out[1]), "flagged": int(out[2]),
             "segments_per_query": int(out[3]), "segment_capacity": int(out[4])}
+
+
+class LengthIndex:
+    """The stored records ordered by input length (sage_length_index), for
+    the semantic-unaware predictor: record indices sorted by length (ties by
+    index), the sorted lengths, and the first sorted position of each length
+    0..max_len+1. Lengths are clamped to [1, max_len]."""
+
+    def __init__(self, hist_prompt_len: torch.Tensor, max_len: int):
+        _dev(hist_prompt_len, torch.int32, "hist_prompt_len", 1)
+        N = hist_prompt_len.shape[0]
+        dev = hist_prompt_len.device
+        self.max_len = int(max_len)
+        self.N = N
+        self.by_len = torch.empty(N, dtype=torch.int32, device=dev)
+        self.sorted_len = torch.empty(N, dtype=torch.int32, device=dev)
+        self.len_off = torch.empty(self.max_len + 2, dtype=torch.int32, device=dev)
+        lib = load_library()
+        ws = torch.empty(max(16, lib.sage_length_index_workspace_bytes(N)), dtype=torch.uint8, device=dev)
+        _check(lib.sage_length_index(hist_prompt_len.data_ptr(), N, self.max_len, self.by_len.data_ptr(),
+                                     self.sorted_len.data_ptr(), self.len_off.data_ptr(), ws.data_ptr(),
+                                     ws.numel(), _stream()))
+        self._ws = ws                                   # alive until the build has run
+
+
+def predict_by_length(prompt_len: torch.Tensor, index: LengthIndex, hist_len: torch.Tensor, k: int, tau: float,
+                      bin_edges: torch.Tensor, out=None):
+    """The semantic-unaware predictor (sage_predict_by_length): neighbours by
+    input-length similarity min/max, then the same histogram as predict."""
+    _dev(prompt_len, torch.int32, "prompt_len", 1)
+    _dev(hist_len, torch.int32, "hist_len", 1)
+    _dev(bin_edges, torch.float64, "bin_edges", 1)
+    Q, B = prompt_len.shape[0], bin_edges.shape[0] - 1
+    dev = prompt_len.device
+    if out is None:
+        out = (torch.empty((Q, k), dtype=torch.int32, device=dev), torch.empty((Q, k), dtype=torch.float32, device=dev),
+               torch.empty((Q, B), dtype=torch.int32, device=dev), torch.empty((Q, B), dtype=torch.float32, device=dev))
+    ids, sims, counts, mass = out
+    _check(load_library().sage_predict_by_length(prompt_len.data_ptr(), Q, index.by_len.data_ptr(),
+                                                 index.sorted_len.data_ptr(), index.len_off.data_ptr(),
+                                                 index.max_len, hist_len.data_ptr(), index.N, int(k), float(tau),
+                                                 bin_edges.data_ptr(), B, ids.data_ptr(), sims.data_ptr(),
+                                                 counts.data_ptr(), mass.data_ptr(), _stream()))
+    return ids, sims, counts, mass
 
 
 CHECK_BITS = {1: "bin edges not finite and strictly increasing",

@@ -261,3 +261,28 @@ def test_predict_noalloc_rejects_before_enqueue(lib):
     assert b"static" in lib.sage_last_error()
     assert fn(A, 1, 4, A, 1, A, 100, 48, 8, 0.8, A, 16, A, A, A, A, None) == SAGE_EINVAL      # d % 32
     assert fn(A, 1, 4, A, 1, A, 100, 64, 0, 0.8, A, 16, A, A, A, A, None) == SAGE_EINVAL      # k
+
+
+def test_length_predictor_validation(lib):
+    P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    bi = lib.sage_length_index
+    bi.argtypes = [P, I, I, P, P, P, P, Z, P]
+    lib.sage_length_index_workspace_bytes.argtypes = [I]
+    lib.sage_length_index_workspace_bytes.restype = Z
+    a = [A + 0x1000 * i for i in range(5)]
+    assert lib.sage_length_index_workspace_bytes(1000) > 4000
+    assert bi(a[0], 0, 100, a[1], a[2], a[3], a[4], 1 << 30, None) == SAGE_EINVAL             # N
+    assert bi(a[0], 10, 0, a[1], a[2], a[3], a[4], 1 << 30, None) == SAGE_EINVAL              # max_len
+    assert bi(a[0], 10, (1 << 20) + 1, a[1], a[2], a[3], a[4], 1 << 30, None) == SAGE_EINVAL
+    assert bi(a[0], 10, 100, None, a[2], a[3], a[4], 1 << 30, None) == SAGE_EINVAL
+    assert bi(a[0], 10, 100, a[1], a[2], a[3], a[4], 0, None) == SAGE_EWORKSPACE
+    pl = lib.sage_predict_by_length
+    pl.argtypes = [P, I, P, P, P, I, P, I, I, F, P, I, P, P, P, P, P]
+    ok = lambda **kw: dict(dict(Q=4, max_len=100, N=10, k=8, tau=0.8, B=16), **kw)
+    def call(**kw):
+        c = ok(**kw)
+        return pl(a[0], c["Q"], a[1], a[2], a[3], c["max_len"], a[4], c["N"], c["k"], c["tau"], A, c["B"],
+                  A, A, A, A, None)
+    for bad in (dict(Q=-1), dict(N=0), dict(k=0), dict(k=257), dict(B=0), dict(max_len=0), dict(tau=0.0)):
+        assert call(**bad) == SAGE_EINVAL, bad
+    assert call(Q=0) == SAGE_OK
