@@ -532,6 +532,10 @@ def run_ttlt(args, torch, sage, workloads):
     host_orders = {pol: (o.cpu().numpy(), L if pol == "gittins" else 1,
                          informed if pol == "gittins" else R, pol == "gittins")
                    for pol, o in orders.items()}
+    # The other reading of a refresh that finds no predicted mass above the
+    # service received: the request ranks last (+inf) instead of keeping its
+    # last index (every entry of the table counts as informed).
+    host_orders["gittins (exhausted last)"] = (host_orders["gittins"][0], L, L * R, True)
     # The same policies on inaccurate predictions (Sec. 4.3: a uniform
     # distribution merged in at 1:4); outside the timed region.
     for pol in ("mean", "gittins-static", "gittins"):
