@@ -296,6 +296,11 @@ def main():
         "stage_rooflines": stage_rooflines(stages, Q, d, k, B, search),
         "search": search,
     }
+    # measured HBM bytes per launch of the stage kernels, where a current counter summary exists
+    for stage, kern, srcs in (("hist", "hist_kernel", ("k_hist.hip", "sage_device.hpp")),
+                              ("topk_select", "select_kernel", ("k_sim_topk.hip", "sage_device.hpp"))):
+        if stage in line["stage_rooflines"]:
+            line["stage_rooflines"][stage]["traffic"] = read_traffic(kern, workload_key, srcs)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)
