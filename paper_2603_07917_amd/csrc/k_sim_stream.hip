@@ -259,6 +259,7 @@ template <int S>
 __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __restrict__ cand,
                                                           const int* __restrict__ cand_count, int cap, int k,
                                                           int need, int* __restrict__ flags,
+                                                          uint32_t* __restrict__ flag_word, uint32_t epoch,
                                                           int32_t* __restrict__ ids, float* __restrict__ sims) {
   constexpr int KL = 64 * S;
   constexpr int W = 16;
@@ -270,7 +271,10 @@ __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __rest
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int n = cand_count[q];
   if (n > cap || n < need) {                         // need = min(k, N)
-    if (tid == 0) flags[q] = 1;
+    if (tid == 0) {
+      flags[q] = 1;
+      *flag_word = epoch;
+    }
     return;
   }
   if (tid == 0) flags[q] = 0;
@@ -353,7 +357,7 @@ hipError_t launch_stream_sample(EmbView queries, int Q, EmbView hist, int N, int
 }
 
 hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int d, int k, int chunk_rows,
-                                const float* theta0, int cap, uint64_t* cand, int* cand_count, int* flags,
+                                const float* theta0, int cap, uint64_t* cand, int* cand_count, Flagged fl,
                                 int32_t* ids, float* sims, hipStream_t stream) {
   if (Q <= 0 || Q > kStreamMaxQ || d % 32 != 0 || d > kStreamMaxD || k > 256 || N <= 0 || chunk_rows <= 0)
     return hipErrorInvalidValue;
@@ -367,13 +371,13 @@ hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int
   LaunchScope scope("topk_select", stream);
   if (k <= 64)
     hipLaunchKernelGGL((select_few_kernel<1>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
-                       min(k, N), flags, ids, sims);
+                       min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
   else if (k <= 128)
     hipLaunchKernelGGL((select_few_kernel<2>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
-                       min(k, N), flags, ids, sims);
+                       min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
   else
     hipLaunchKernelGGL((select_few_kernel<4>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
-                       min(k, N), flags, ids, sims);
+                       min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
   return hipGetLastError();
 }
 

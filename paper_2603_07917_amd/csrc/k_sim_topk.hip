@@ -26,6 +26,8 @@
 //   between when a step brings more), and the wave owning the query folds
 //   full buffers into the query's descending list with a bitonic merge. The
 //   lists end in the partial buffer [Q][chunks][KL].
+#include <atomic>
+
 #include "sage_device.hpp"
 #include "sage_internal.hpp"
 
@@ -237,21 +239,20 @@ struct TopkSmem {
   int rounds;
 };
 
+// One (query tile, history chunk) of the list search.
 template <int NQT, int KL>
-__global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
-    EmbView queries, int Q, EmbView hist, int N, int d,
-    int k, int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0,
-    const int* __restrict__ only_flagged, uint64_t* __restrict__ partial) {
+__device__ __forceinline__ void list_tile(TopkSmem<NQT, KL>& sm, EmbView queries, int Q, EmbView hist, int N,
+                                          int d, int k, int chunk_rows, int n_chunks, int q_tiles,
+                                          const float* __restrict__ theta0, const int* __restrict__ only_flagged,
+                                          uint64_t* __restrict__ partial, const int b) {
   constexpr int BQ = 32 * NQT;
   constexpr int QPW = BQ / 4;              // queries merged by each wave
   constexpr int kCap = CapOf<NQT>::value;
-  __shared__ __align__(16) TopkSmem<NQT, KL> sm;
 
   // Block -> (query tile, chunk). When the chunks split evenly over the 8
   // XCDs, the query tiles of one chunk are dispatched to the same XCD so that
   // its history rows are shared through that XCD's L2.
   int qt, chunk;
-  const int b = blockIdx.x;
   if (n_chunks % 8 == 0) {
     const int x = b & 7, slot = b >> 3;
     chunk = x + 8 * (slot / q_tiles);
@@ -399,6 +400,25 @@ __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     if (q < Q) partial[((size_t)q * n_chunks + chunk) * KL + e] = sm.list[i];
   }
 }
+
+template <int NQT, int KL>
+__global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
+    EmbView queries, int Q, EmbView hist, int N, int d,
+    int k, int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0,
+    const int* __restrict__ only_flagged, const uint32_t* __restrict__ flag_word, uint32_t epoch,
+    uint64_t* __restrict__ partial) {
+  __shared__ __align__(16) TopkSmem<NQT, KL> sm;
+  // As the exact fallback: nothing to do unless a query of this call was
+  // flagged (the flagging kernel stored this call's epoch in the word).
+  if (only_flagged && *flag_word != epoch) return;
+  // Tiles b = blockIdx.x, + gridDim.x, ... (one each for the full search).
+  for (int b = blockIdx.x; b < q_tiles * n_chunks; b += gridDim.x) {
+    __syncthreads();                         // the previous tile's LDS reads are done
+    list_tile<NQT, KL>(sm, queries, Q, hist, N, d, k, chunk_rows, n_chunks, q_tiles, theta0, only_flagged,
+                       partial, b);
+  }
+}
+
 
 
 // Descending order of a bitonic sequence held one key per lane (half-cleaners).
@@ -952,6 +972,7 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
 __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict__ seg,
                                                      const int* __restrict__ seg_count, int Q, int n_chunks,
                                                      int seg_cap, int k, int need, int* __restrict__ flags,
+                                                     uint32_t* __restrict__ flag_word, uint32_t epoch,
                                                      int32_t* __restrict__ ids, float* __restrict__ sims) {
   __shared__ int off_s[4][kWave + 1];
   __shared__ uint64_t pend[4][2 * kWave];
@@ -976,7 +997,10 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
   // keys beat theta0: the pre-pass scores are the filter's own, bit for
   // bit, so the latter only follows from a raised threshold.
   if (__any(n > seg_cap) || total < need) {
-    if (lane == 0) flags[q] = 1;
+    if (lane == 0) {
+      flags[q] = 1;
+      *flag_word = epoch;
+    }
     return;
   }
   if (lane == 0) flags[q] = 0;
@@ -1032,12 +1056,16 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
 
 template <int NQT, int KL>
 hipError_t launch_lists(EmbView queries, int Q, EmbView hist, int N, int d, int k,
-                        const SimTopkPlan& p, const float* theta0, const int* only_flagged,
+                        const SimTopkPlan& p, const float* theta0, const Flagged* only_flagged,
                         uint64_t* partial, hipStream_t stream) {
   LaunchScope scope(only_flagged ? "sim_topk_fallback" : "sim_topk", stream);
-  hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), dim3(p.q_tiles * p.n_chunks), dim3(kThreads), 0,
-                     stream, queries, Q, hist, N, d, k, p.chunk_rows, p.n_chunks, p.q_tiles, theta0,
-                     only_flagged, partial);
+  // The fallback runs as one round of workgroups (one per CU) that loop over
+  // the tiles, and return at once when no query of the call was flagged.
+  const int tiles = p.q_tiles * p.n_chunks;
+  hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), dim3(only_flagged ? std::min(tiles, 256) : tiles), dim3(kThreads),
+                     0, stream, queries, Q, hist, N, d, k, p.chunk_rows, p.n_chunks, p.q_tiles, theta0,
+                     only_flagged ? only_flagged->flags : nullptr, only_flagged ? only_flagged->word : nullptr,
+                     only_flagged ? only_flagged->epoch : 0u, partial);
   return hipGetLastError();
 }
 
@@ -1115,6 +1143,11 @@ void chunking(int q_tiles, int N, int target_blocks, int max_chunks, int* chunk_
 
 }  // namespace
 
+uint32_t next_epoch() {
+  static std::atomic<uint32_t> counter{0};
+  return counter.fetch_add(1u, std::memory_order_relaxed) + 1u;
+}
+
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   SimTopkPlan p{};
   int L = 64;
@@ -1185,11 +1218,13 @@ SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
     p.off_seg = o;    o = align256(o + (size_t)Q * p.f_n_chunks * p.seg_cap * sizeof(uint64_t));
     p.off_segcnt = o; o = align256(o + (size_t)Q * p.f_n_chunks * sizeof(int));
     p.off_flags = o;  o = align256(o + (size_t)Q * sizeof(int));
+    p.off_flag_word = o; o = align256(o + sizeof(uint32_t));
   }
   if (p.stream) {
     p.off_cand = o;   o = align256(o + (size_t)Q * p.s_cap * sizeof(uint64_t));
     p.off_ccount = o; o = align256(o + (size_t)Q * sizeof(int));
     p.off_flags = o;  o = align256(o + (size_t)Q * sizeof(int));
+    p.off_flag_word = o; o = align256(o + sizeof(uint32_t));
   }
   p.total_bytes = o;
   return p;
@@ -1212,7 +1247,8 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     }
     uint64_t* seg = reinterpret_cast<uint64_t*>(ws + p.off_seg);
     int* segcnt = reinterpret_cast<int*>(ws + p.off_segcnt);
-    int* flags = reinterpret_cast<int*>(ws + p.off_flags);
+    const Flagged fl{reinterpret_cast<int*>(ws + p.off_flags), reinterpret_cast<uint32_t*>(ws + p.off_flag_word),
+                     next_epoch()};
     {
       LaunchScope scope("sim_topk", stream);
       hipLaunchKernelGGL(sim_filter_kernel, dim3(p.f_q_tiles * p.f_n_chunks), dim3(kThreads), 0, stream,
@@ -1222,28 +1258,29 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     {
       LaunchScope scope("topk_select", stream);
       hipLaunchKernelGGL(select_kernel, dim3((Q + 3) / 4), dim3(256), 0, stream, seg, segcnt, Q,
-                         p.f_n_chunks, p.seg_cap, k, min(k, N), flags, ids, sims);
+                         p.f_n_chunks, p.seg_cap, k, min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
     }
     // Exact fallback for queries whose candidates overflowed (no work otherwise).
-    e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
+    e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, &fl, partial, stream);
     if (e != hipSuccess) return e;
-    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, merge_lists, ids, sims, stream);
+    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, &fl, merge_lists, ids, sims, stream);
   }
   if (p.stream) {
     uint64_t* cand = reinterpret_cast<uint64_t*>(ws + p.off_cand);
     int* ccount = reinterpret_cast<int*>(ws + p.off_ccount);
-    int* flags = reinterpret_cast<int*>(ws + p.off_flags);
+    const Flagged fl{reinterpret_cast<int*>(ws + p.off_flags), reinterpret_cast<uint32_t*>(ws + p.off_flag_word),
+                     next_epoch()};
     e = launch_theta(queries, Q, hist, N, d, k, p, 1, Sampler::stream, gm, theta0, ccount, stream);
     if (e != hipSuccess) return e;
-    e = launch_stream_search(queries, Q, hist, N, d, k, p.s_chunk_rows, theta0, p.s_cap, cand, ccount, flags,
+    e = launch_stream_search(queries, Q, hist, N, d, k, p.s_chunk_rows, theta0, p.s_cap, cand, ccount, fl,
                              ids, sims, stream);
     if (e != hipSuccess) return e;
     // Exact fallback for queries whose candidates overflowed (no work otherwise).
-    if (p.list_len == 64) e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
-    else if (p.list_len == 128) e = launch_lists<2, 128>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
-    else e = launch_lists<1, 256>(queries, Q, hist, N, d, k, p, nullptr, flags, partial, stream);
+    if (p.list_len == 64) e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, &fl, partial, stream);
+    else if (p.list_len == 128) e = launch_lists<2, 128>(queries, Q, hist, N, d, k, p, nullptr, &fl, partial, stream);
+    else e = launch_lists<1, 256>(queries, Q, hist, N, d, k, p, nullptr, &fl, partial, stream);
     if (e != hipSuccess) return e;
-    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, flags, merge_lists, ids, sims, stream);
+    return launch_topk_merge(partial, Q, p.n_chunks, p.list_len, k, &fl, merge_lists, ids, sims, stream);
   }
   if (p.n_samples > 0) {
     e = launch_theta(queries, Q, hist, N, d, k, p, p.q_tiles, Sampler::list, gm, theta0, nullptr, stream);

@@ -19,13 +19,10 @@ constexpr int kMergeKeys = 4096;   // LDS capacity in keys (32 KiB)
 // when gridDim.y == 1). With `out_lists` it writes the merged list of L keys
 // to out_lists[q][y] (first level of a two-level merge); otherwise the first
 // k entries as ids and similarities.
-__global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
-    const uint64_t* __restrict__ partial, int n_lists, int list_len, int k, int per_group,
-    const int* __restrict__ only_flagged, uint64_t* __restrict__ out_lists, int32_t* __restrict__ ids,
-    float* __restrict__ sims) {
-  __shared__ uint64_t slot[kMergeKeys];
-  const int q = blockIdx.x;
-  if (only_flagged && only_flagged[q] == 0) return;
+__device__ __forceinline__ void merge_query(uint64_t* slot, int q, const uint64_t* __restrict__ partial,
+                                            int n_lists, int list_len, int k, int per_group,
+                                            uint64_t* __restrict__ out_lists, int32_t* __restrict__ ids,
+                                            float* __restrict__ sims) {
   const int L = list_len;
   const int G = kMergeKeys / L;                 // lists per LDS batch (power of two)
   const int first = blockIdx.y * per_group;
@@ -81,24 +78,45 @@ __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
   }
 }
 
+// Queries q = blockIdx.x, + gridDim.x, ... As the exact fallback (with
+// only_flagged) it returns at once unless a query of this call was flagged,
+// and merges only the flagged queries.
+__global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
+    const uint64_t* __restrict__ partial, int Q, int n_lists, int list_len, int k, int per_group,
+    const int* __restrict__ only_flagged, const uint32_t* __restrict__ flag_word, uint32_t epoch,
+    uint64_t* __restrict__ out_lists, int32_t* __restrict__ ids, float* __restrict__ sims) {
+  __shared__ uint64_t slot[kMergeKeys];
+  if (only_flagged && *flag_word != epoch) return;
+  for (int q = blockIdx.x; q < Q; q += gridDim.x) {
+    if (only_flagged && only_flagged[q] == 0) continue;
+    __syncthreads();                            // the previous query's LDS reads are done
+    merge_query(slot, q, partial, n_lists, list_len, k, per_group, out_lists, ids, sims);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
-                             const int* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
+                             const Flagged* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
                              hipStream_t stream) {
   if (Q == 0) return hipSuccess;
   LaunchScope scope(only_flagged ? "topk_merge_fallback" : "topk_merge", stream);
+  const int* flags = only_flagged ? only_flagged->flags : nullptr;
+  const uint32_t* word = only_flagged ? only_flagged->word : nullptr;
+  const uint32_t epoch = only_flagged ? only_flagged->epoch : 0u;
+  // One workgroup per query; as the fallback, at most 1024 that loop over the queries.
+  const int gx = only_flagged ? std::min(Q, 1024) : Q;
   const int groups = merge_groups(Q, n_lists, list_len);
   if (groups > 1 && scratch_lists) {
     // Few queries with many lists: merge groups of lists in parallel first.
     const int per_group = (n_lists + groups - 1) / groups;
-    hipLaunchKernelGGL(topk_merge_kernel, dim3(Q, groups), dim3(kMergeThreads), 0, stream, partial,
-                       n_lists, list_len, k, per_group, only_flagged, scratch_lists, nullptr, nullptr);
-    hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, scratch_lists, groups,
-                       list_len, k, groups, only_flagged, nullptr, ids, sims);
+    hipLaunchKernelGGL(topk_merge_kernel, dim3(gx, groups), dim3(kMergeThreads), 0, stream, partial, Q,
+                       n_lists, list_len, k, per_group, flags, word, epoch, scratch_lists, nullptr, nullptr);
+    hipLaunchKernelGGL(topk_merge_kernel, dim3(gx), dim3(kMergeThreads), 0, stream, scratch_lists, Q, groups,
+                       list_len, k, groups, flags, word, epoch, nullptr, ids, sims);
   } else {
-    hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(kMergeThreads), 0, stream, partial, n_lists,
-                       list_len, k, n_lists, only_flagged, nullptr, ids, sims);
+    hipLaunchKernelGGL(topk_merge_kernel, dim3(gx), dim3(kMergeThreads), 0, stream, partial, Q, n_lists,
+                       list_len, k, n_lists, flags, word, epoch, nullptr, ids, sims);
   }
   return hipGetLastError();
 }

@@ -59,7 +59,7 @@ struct SimTopkPlan {
   int s_chunk_rows; // history rows per workgroup
   int s_cap;        // candidate keys per query
   // workspace layout (byte offsets, 256-aligned)
-  size_t off_partial, off_merge, off_gm, off_theta, off_seg, off_segcnt, off_flags, off_cand, off_ccount,
+  size_t off_partial, off_merge, off_gm, off_theta, off_seg, off_segcnt, off_flags, off_flag_word, off_cand, off_ccount,
       total_bytes;
   size_t workspace_bytes() const { return total_bytes; }
 };
@@ -73,8 +73,20 @@ hipError_t launch_stream_sample(EmbView queries, int Q, EmbView hist, int N, int
 // Test hook (sage_debug_theta_floor): a floor on the pre-pass threshold of the
 // filtered and stream paths; -inf when unset.
 float debug_theta_floor();
+// Queries sent to the exact fallback: flags[q] = 1 for each, and the
+// flagging kernel stores `epoch` (a value new to each call) in *word once any
+// query is flagged, so that the fallback kernels return at once when the word
+// holds another value. A stale word that matches costs time, never results:
+// the fallback still works from the flags.
+struct Flagged {
+  int* flags;
+  uint32_t* word;
+  uint32_t epoch;
+};
+uint32_t next_epoch();
+
 hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int d, int k, int chunk_rows,
-                                const float* theta0, int cap, uint64_t* cand, int* cand_count, int* flags,
+                                const float* theta0, int cap, uint64_t* cand, int* cand_count, Flagged fl,
                                 int32_t* ids, float* sims, hipStream_t stream);
 
 // Launchers: each enqueues kernels on `stream` and returns the HIP status of
@@ -119,7 +131,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
 // Number of first-level groups of the list merge (1: single level).
 int merge_groups(int Q, int n_lists, int list_len);
 hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int list_len, int k,
-                             const int* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
+                             const Flagged* only_flagged, uint64_t* scratch_lists, int32_t* ids, float* sims,
                              hipStream_t stream);
 hipError_t launch_hist(const int32_t* ids, const float* sims, int Q, int k, const int32_t* hist_len,
                        int N, float tau, const double* edges, int B, int uniform, int32_t* counts,
