@@ -99,6 +99,33 @@ def stage_rooflines(stages, rows_per_launch: float, d: int, k: int, B: int, sear
     return out
 
 
+def timed_steps(step, steps: int, label: str, sage, torch, capacity: int = 64):
+    """Wall time of `steps` calls of step(i), with HIP events recorded only
+    around the launches named `label` (the dominant kernel, whose duration the
+    roofline needs) so that the timed work is otherwise the untimed one; then
+    `steps` more calls with every launch timed, for the per-stage split.
+    Returns (elapsed seconds, (launches, ms) of `label`, {stage: (launches, ms)}
+    of the second pass)."""
+    timer = sage.StageTimer(capacity=capacity * (steps + 1), only=label)
+    with timer:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(i)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    dominant = timer.totals()[label]
+    timer.close()
+    split = sage.StageTimer(capacity=capacity * (steps + 1))
+    with split:
+        for i in range(steps):
+            step(steps + i)
+        torch.cuda.synchronize()
+    stages = split.totals()
+    split.close()
+    return elapsed, dominant, stages
+
+
 def kernel_name(k: int, Q: int = 1 << 30) -> str:
     """The kernel behind the `sim_topk` timer label: the stream search for at
     most 16 queries (large stores), else the filtered path for k <= 64."""
@@ -251,22 +278,12 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    timer = sage.StageTimer(capacity=64 * (args.steps + 1))
-    with timer:
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t0
-    stages = timer.totals()
-    timer.close()
+    elapsed, (n_launch, k1_ms), stages = timed_steps(lambda i: step(), args.steps, "sim_topk", sage, torch)
     print(f"# step: {1e3 * elapsed / args.steps:.3f} ms", file=sys.stderr, flush=True)
-    search = sage.predict_stats(ws, Q, N, d, k, B)      # the last (timed) step's search; synchronises
+    search = sage.predict_stats(ws, Q, N, d, k, B)      # the last step's search (same inputs); synchronises
 
     ms_per_step = 1e3 * elapsed / args.steps
     value = Q * args.steps / elapsed
-    n_launch, k1_ms = stages["sim_topk"]
     k1_avg_s = k1_ms / n_launch / 1e3
     flops = 2.0 * Q * N * d
     achieved = flops / k1_avg_s / 1e12
@@ -325,17 +342,7 @@ def run_index_bound(args, torch, sage, workloads):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    timer = sage.StageTimer(capacity=64 * (args.steps + 1))
-    with timer:
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t0
-    stages = timer.totals()
-    timer.close()
-    n_launch, k_ms = stages["index_scan"]
+    elapsed, (n_launch, k_ms), stages = timed_steps(lambda i: step(), args.steps, "index_scan", sage, torch)
     avg_s = k_ms / n_launch / 1e3
     k_bytes = Q * (4.0 * B + 8.0)               # masses + prompt lengths in, index out
     achieved = k_bytes / avg_s / 1e9
@@ -418,20 +425,16 @@ def run_streaming(args, torch, sage, workloads):
     log("timed calls")
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    timer = sage.StageTimer(capacity=64 * (args.steps + 1))
-    with timer:
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(args.steps):
+    def timed_call(i):
+        if i < args.steps:
             starts[i].record()
             call(args.warmup + i)
             ends[i].record()
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t0
-    stages = timer.totals()
-    timer.close()
+        else:
+            call(args.warmup + i)
+
+    elapsed, (n_launch, k1_ms), stages = timed_steps(timed_call, args.steps, "sim_topk", sage, torch)
     lat = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
-    n_launch, k1_ms = stages["sim_topk"]
     k1_avg_s = k1_ms / n_launch / 1e3
     k1_bytes = 2.0 * spec.N * spec.d + 2.0 * batch * spec.d
     achieved = k1_bytes / k1_avg_s / 1e9
@@ -521,16 +524,8 @@ def run_ttlt(args, torch, sage, workloads):
         step()
     torch.cuda.synchronize()
     log("timed passes")
-    timer = sage.StageTimer(capacity=(L + 64) * (args.steps + 1))
-    with timer:
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t0
-    stages = timer.totals()
-    timer.close()
+    elapsed, (n_launch, k1_ms), stages = timed_steps(lambda i: step(), args.steps, "sim_topk", sage, torch,
+                                                     capacity=L + 64)
 
     log("replaying the trace")
     informed = int(np.isfinite(table.cpu().numpy()).sum())
@@ -583,7 +578,6 @@ def run_ttlt(args, torch, sage, workloads):
     rate1 = simulator.rate_for_load(tr.prompt_len, tr.output_len, 8.0, 1, args.load)
     single = replay(tr.arrival * nodes, 1, rate1)
 
-    n_launch, k1_ms = stages["sim_topk"]
     k1_avg_s = k1_ms / n_launch / 1e3
     rows = R / n_launch * args.steps                 # queries per predict launch (chunked)
     flops = 2.0 * rows * spec.N * spec.d

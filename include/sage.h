@@ -517,6 +517,10 @@ typedef struct sage_timer sage_timer;
 int sage_timer_create(int capacity, sage_timer** out);
 int sage_timer_destroy(sage_timer* t);
 int sage_timer_attach(sage_timer* t);   /* NULL detaches */
+/* Time only the launches named `label` (a kernel name as sage_timer_get
+ * reports it); NULL or "" times every launch again. Fewer events keep the
+ * timed work closer to the untimed one. Host string, copied. */
+int sage_timer_only(sage_timer* t, const char* label);
 int sage_timer_reset(sage_timer* t);
 /* Number of distinct kernel names seen since the last reset. */
 int sage_timer_count(sage_timer* t);

@@ -88,12 +88,13 @@ struct sage_timer {
   int used = 0;
   std::vector<hipEvent_t> start, stop;
   std::vector<const char*> name;
+  std::string only;          // when set, only launches of this name are timed
 };
 
 namespace sage {
 LaunchScope::LaunchScope(const char* name, hipStream_t stream) : stream_(stream) {
   sage_timer* t = g_timer;
-  if (!t || t->used >= t->capacity) return;
+  if (!t || t->used >= t->capacity || (!t->only.empty() && t->only != name)) return;
   slot_ = t->used++;
   t->name[slot_] = name;
   (void)hipEventRecord(t->start[slot_], stream);
@@ -138,6 +139,12 @@ SAGE_API int sage_timer_destroy(sage_timer* t) {
 
 SAGE_API int sage_timer_attach(sage_timer* t) {
   g_timer = t;
+  return ok();
+}
+
+SAGE_API int sage_timer_only(sage_timer* t, const char* label) {
+  if (!t) return fail(SAGE_EINVAL, "timer is NULL");
+  t->only = label ? label : "";
   return ok();
 }
 

@@ -67,6 +67,7 @@ def load_library():
         "sage_timer_create": (I, [I, ctypes.POINTER(P)]),
         "sage_timer_destroy": (I, [P]),
         "sage_timer_attach": (I, [P]),
+        "sage_timer_only": (I, [P, ctypes.c_char_p]),
         "sage_timer_reset": (I, [P]),
         "sage_timer_count": (I, [P]),
         "sage_timer_get": (I, [P, I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I),
@@ -631,13 +632,16 @@ class Queue:
 
 
 class StageTimer:
-    """Per-kernel HIP-event timing of everything the library launches while attached."""
+    """Per-kernel HIP-event timing of what the library launches while attached:
+    every launch, or only those named `only`."""
 
-    def __init__(self, capacity: int = 4096):
+    def __init__(self, capacity: int = 4096, only: str | None = None):
         lib = load_library()
         h = ctypes.c_void_p()
         _check(lib.sage_timer_create(capacity, ctypes.byref(h)))
         self._h = h
+        if only:
+            _check(lib.sage_timer_only(h, only.encode()))
 
     def __enter__(self):
         _check(load_library().sage_timer_attach(self._h))
