@@ -159,3 +159,54 @@ def test_store_rejects_unsorted_bins():
     with pytest.raises(sage.SageError, match="representatives"):
         sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(r), 8)
     sage.Store(dev(w.hist_emb), dev(w.hist_len), dev(w.bin_edges), dev(w.bin_repr), 8)   # fine
+
+
+@pytest.mark.parametrize("Q,k", [(300, 32), (8, 64)])
+def test_fallback_word_from_an_earlier_call(Q, k):
+    """One workspace for a call that flags queries (theta0 raised from the
+    host) and then for calls that flag none: the word the flagging call left
+    holds an older call's value, so the later calls' fallback launches return
+    at once, and their results equal the oracle's and the first unforced
+    call's bit for bit."""
+    N, d = 60000, 64
+    print(f"case Q={Q} k={k}", flush=True)
+    w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=32, seed=900 + Q + k, clusters=5)
+    qb = sage.ingest_bf16(dev(w.queries), "panels")
+    hb = sage.ingest_bf16(dev(w.hist_emb), "panels")
+    hl, be = dev(w.hist_len), dev(w.bin_edges)
+    ws = torch.empty(sage.predict_workspace_bytes(Q, N, d, k, 32), dtype=torch.uint8, device="cuda")
+    S = oracle_scores(w)
+    base = [host(t) for t in sage.predict(qb, hb, hl, k, 0.8, be, workspace=ws)]
+    parity.check_predict(*base, S, w.hist_len, w.bin_edges, 0.8, k)
+    try:
+        sage.debug_theta_floor(2.0)                  # every query flagged
+        forced = [host(t) for t in sage.predict(qb, hb, hl, k, 0.8, be, workspace=ws)]
+    finally:
+        sage.debug_theta_floor(-np.inf)
+    parity.check_predict(*forced, S, w.hist_len, w.bin_edges, 0.8, k)
+    for _ in range(2):
+        again = [host(t) for t in sage.predict(qb, hb, hl, k, 0.8, be, workspace=ws)]
+        for a, b in zip(base, again):
+            assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+def test_timer_only_times_the_named_launches():
+    w = workloads.small_predict(Q=64, N=20000, d=64, k=16, B=32, seed=11, clusters=4)
+    qb = sage.ingest_bf16(dev(w.queries), "panels")
+    hb = sage.ingest_bf16(dev(w.hist_emb), "panels")
+    hl, be = dev(w.hist_len), dev(w.bin_edges)
+    torch.cuda.synchronize()
+    full = sage.StageTimer(capacity=256)
+    with full:
+        sage.predict(qb, hb, hl, 16, 0.8, be)
+        torch.cuda.synchronize()
+    names = set(full.totals())
+    full.close()
+    assert {"sim_topk", "hist"} <= names
+    only = sage.StageTimer(capacity=256, only="hist")
+    with only:
+        sage.predict(qb, hb, hl, 16, 0.8, be)
+        torch.cuda.synchronize()
+    got = only.totals()
+    only.close()
+    assert set(got) == {"hist"} and got["hist"][0] == 1 and got["hist"][1] > 0.0
