@@ -21,6 +21,8 @@ from tests import parity
 
 pytestmark = pytest.mark.gpu
 
+STREAM_MAX_D = 2048          # the stream path takes d up to this
+
 
 def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
@@ -44,14 +46,15 @@ def oracle_scores(w):
 
 def sample_every(Q, N, d, k):
     """The pre-pass's step stride as the library plans it: every SR-th whole
-    256-row step, SR chosen for >= 4k group maxima (16 per step), at most 16
-    for k <= 64 on a store below 2^29 elements (or few queries), else 32, and
-    at most 512 sampled steps."""
+    256-row step, SR chosen for >= 4k group maxima (16 per step), at most 128
+    on the stream path (at most 16 queries), else at most 16 for k <= 64 on a
+    store below 2^29 elements and 32 otherwise, and at most 512 sampled steps."""
     steps = N // 256
     L = max(64, 1 << (k - 1).bit_length())
     assert steps * 16 >= 8 * k, "store too small for a pre-pass"
     wide = Q > 16 and N * d >= (1 << 29)
-    sr_max = 16 if (L == 64 and not wide) else 32
+    few = Q <= 16 and d <= STREAM_MAX_D and k <= 256
+    sr_max = 128 if few else (16 if (L == 64 and not wide) else 32)
     sr = max(1, min(sr_max, steps * 16 // (4 * k)))
     while -(-steps // sr) > 512:
         sr += 1
