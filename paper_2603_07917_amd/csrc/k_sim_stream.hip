@@ -98,8 +98,9 @@ __global__ void __launch_bounds__(kThreads) stream_sample_kernel(EmbView queries
 // l % 16.
 __global__ void __launch_bounds__(kThreads) sim_stream_kernel(
     EmbView queries, int Q, EmbView hist, int N, int d, int chunk_rows, const float* __restrict__ theta0,
-    int cap, uint64_t* __restrict__ cand, int* __restrict__ cand_count) {
+    int cap, uint64_t* __restrict__ cand, int* __restrict__ cand_count, uint32_t* __restrict__ flag_word) {
   extern __shared__ uint4 qfrag[];                  // d / 32 KiB, sized at launch
+  if (blockIdx.x == 0 && threadIdx.x == 0) *flag_word = 0u;     // set again by the select if it flags a query
   __shared__ uint64_t lbuf[kStreamMaxQ][kLCap];
   __shared__ int lcnt[kStreamMaxQ];
   __shared__ int gbase[kStreamMaxQ];
@@ -259,7 +260,7 @@ template <int S>
 __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __restrict__ cand,
                                                           const int* __restrict__ cand_count, int cap, int k,
                                                           int need, int* __restrict__ flags,
-                                                          uint32_t* __restrict__ flag_word, uint32_t epoch,
+                                                          uint32_t* __restrict__ flag_word,
                                                           int32_t* __restrict__ ids, float* __restrict__ sims) {
   constexpr int KL = 64 * S;
   constexpr int W = 16;
@@ -273,7 +274,7 @@ __global__ void __launch_bounds__(1024) select_few_kernel(const uint64_t* __rest
   if (n > cap || n < need) {                         // need = min(k, N)
     if (tid == 0) {
       flags[q] = 1;
-      *flag_word = epoch;
+      *flag_word = 1u;
     }
     return;
   }
@@ -366,18 +367,18 @@ hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int
     const int blocks = (N + chunk_rows - 1) / chunk_rows;
     const size_t lds = (size_t)(d / 32) * kWave * sizeof(uint4);   // sized to d: more workgroups per CU
     hipLaunchKernelGGL(sim_stream_kernel, dim3(blocks), dim3(kThreads), lds, stream, queries, Q, hist, N, d,
-                       chunk_rows, theta0, cap, cand, cand_count);
+                       chunk_rows, theta0, cap, cand, cand_count, fl.word);
   }
   LaunchScope scope("topk_select", stream);
   if (k <= 64)
     hipLaunchKernelGGL((select_few_kernel<1>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
-                       min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
+                       min(k, N), fl.flags, fl.word, ids, sims);
   else if (k <= 128)
     hipLaunchKernelGGL((select_few_kernel<2>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
-                       min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
+                       min(k, N), fl.flags, fl.word, ids, sims);
   else
     hipLaunchKernelGGL((select_few_kernel<4>), dim3(Q), dim3(1024), 0, stream, cand, cand_count, cap, k,
-                       min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
+                       min(k, N), fl.flags, fl.word, ids, sims);
   return hipGetLastError();
 }
 

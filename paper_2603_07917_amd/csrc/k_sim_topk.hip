@@ -405,12 +405,12 @@ template <int NQT, int KL>
 __global__ void __launch_bounds__(kThreads, 1) sim_topk_kernel(
     EmbView queries, int Q, EmbView hist, int N, int d,
     int k, int chunk_rows, int n_chunks, int q_tiles, const float* __restrict__ theta0,
-    const int* __restrict__ only_flagged, const uint32_t* __restrict__ flag_word, uint32_t epoch,
+    const int* __restrict__ only_flagged, const uint32_t* __restrict__ flag_word,
     uint64_t* __restrict__ partial) {
   __shared__ __align__(16) TopkSmem<NQT, KL> sm;
   // As the exact fallback: nothing to do unless a query of this call was
-  // flagged (the flagging kernel stored this call's epoch in the word).
-  if (only_flagged && *flag_word != epoch) return;
+  // flagged (the flagging kernel set the word).
+  if (only_flagged && *flag_word == 0u) return;
   // Tiles b = blockIdx.x, + gridDim.x, ... (one each for the full search).
   for (int b = blockIdx.x; b < q_tiles * n_chunks; b += gridDim.x) {
     __syncthreads();                         // the previous tile's LDS reads are done
@@ -793,8 +793,9 @@ __global__ void __launch_bounds__(kThreads, 1) threshold_sample_ring_kernel(
 __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
     EmbView queries, int Q, EmbView hist, int N, int d,
     int chunk_rows, int n_chunks, int q_tiles, int q_groups, const float* __restrict__ theta0,
-    int seg_cap, uint64_t* __restrict__ seg, int* __restrict__ seg_count) {
+    int seg_cap, uint64_t* __restrict__ seg, int* __restrict__ seg_count, uint32_t* __restrict__ flag_word) {
   __shared__ __align__(16) char lds[ring::kStages * ring::kStageBytes];
+  if (blockIdx.x == 0 && threadIdx.x == 0) *flag_word = 0u;     // set again by the select if it flags a query
   __shared__ int cnt[ring::kBQ];
   // Per-lane rows for reading survivors back by a lane-varying index (16
   // scores each, padded to 80 bytes so that the 16-byte writes of 16 lanes
@@ -972,7 +973,7 @@ __global__ void __launch_bounds__(kThreads, 1) sim_filter_kernel(
 __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict__ seg,
                                                      const int* __restrict__ seg_count, int Q, int n_chunks,
                                                      int seg_cap, int k, int need, int* __restrict__ flags,
-                                                     uint32_t* __restrict__ flag_word, uint32_t epoch,
+                                                     uint32_t* __restrict__ flag_word,
                                                      int32_t* __restrict__ ids, float* __restrict__ sims) {
   __shared__ int off_s[4][kWave + 1];
   __shared__ uint64_t pend[4][2 * kWave];
@@ -999,7 +1000,7 @@ __global__ void __launch_bounds__(256) select_kernel(const uint64_t* __restrict_
   if (__any(n > seg_cap) || total < need) {
     if (lane == 0) {
       flags[q] = 1;
-      *flag_word = epoch;
+      *flag_word = 1u;
     }
     return;
   }
@@ -1065,7 +1066,7 @@ hipError_t launch_lists(EmbView queries, int Q, EmbView hist, int N, int d, int 
   hipLaunchKernelGGL((sim_topk_kernel<NQT, KL>), dim3(only_flagged ? std::min(tiles, 256) : tiles), dim3(kThreads),
                      0, stream, queries, Q, hist, N, d, k, p.chunk_rows, p.n_chunks, p.q_tiles, theta0,
                      only_flagged ? only_flagged->flags : nullptr, only_flagged ? only_flagged->word : nullptr,
-                     only_flagged ? only_flagged->epoch : 0u, partial);
+                     partial);
   return hipGetLastError();
 }
 
@@ -1143,10 +1144,6 @@ void chunking(int q_tiles, int N, int target_blocks, int max_chunks, int* chunk_
 
 }  // namespace
 
-uint32_t next_epoch() {
-  static std::atomic<uint32_t> counter{0};
-  return counter.fetch_add(1u, std::memory_order_relaxed) + 1u;
-}
 
 SimTopkPlan plan_sim_topk(int Q, int N, int d, int k) {
   SimTopkPlan p{};
@@ -1251,18 +1248,17 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
     }
     uint64_t* seg = reinterpret_cast<uint64_t*>(ws + p.off_seg);
     int* segcnt = reinterpret_cast<int*>(ws + p.off_segcnt);
-    const Flagged fl{reinterpret_cast<int*>(ws + p.off_flags), reinterpret_cast<uint32_t*>(ws + p.off_flag_word),
-                     next_epoch()};
+    const Flagged fl{reinterpret_cast<int*>(ws + p.off_flags), reinterpret_cast<uint32_t*>(ws + p.off_flag_word)};
     {
       LaunchScope scope("sim_topk", stream);
       hipLaunchKernelGGL(sim_filter_kernel, dim3(p.f_q_tiles * p.f_n_chunks), dim3(kThreads), 0, stream,
                          queries, Q, hist, N, d, p.f_chunk_rows, p.f_n_chunks, p.f_q_tiles, p.f_q_groups,
-                         p.n_samples > 0 ? theta0 : nullptr, p.seg_cap, seg, segcnt);
+                         p.n_samples > 0 ? theta0 : nullptr, p.seg_cap, seg, segcnt, fl.word);
     }
     {
       LaunchScope scope("topk_select", stream);
       hipLaunchKernelGGL(select_kernel, dim3((Q + 3) / 4), dim3(256), 0, stream, seg, segcnt, Q,
-                         p.f_n_chunks, p.seg_cap, k, min(k, N), fl.flags, fl.word, fl.epoch, ids, sims);
+                         p.f_n_chunks, p.seg_cap, k, min(k, N), fl.flags, fl.word, ids, sims);
     }
     // Exact fallback for queries whose candidates overflowed (no work otherwise).
     e = launch_lists<4, 64>(queries, Q, hist, N, d, k, p, nullptr, &fl, partial, stream);
@@ -1272,8 +1268,7 @@ hipError_t launch_neighbours(EmbView queries, int Q, EmbView hist, int N, int d,
   if (p.stream) {
     uint64_t* cand = reinterpret_cast<uint64_t*>(ws + p.off_cand);
     int* ccount = reinterpret_cast<int*>(ws + p.off_ccount);
-    const Flagged fl{reinterpret_cast<int*>(ws + p.off_flags), reinterpret_cast<uint32_t*>(ws + p.off_flag_word),
-                     next_epoch()};
+    const Flagged fl{reinterpret_cast<int*>(ws + p.off_flags), reinterpret_cast<uint32_t*>(ws + p.off_flag_word)};
     e = launch_theta(queries, Q, hist, N, d, k, p, 1, Sampler::stream, gm, theta0, ccount, stream);
     if (e != hipSuccess) return e;
     e = launch_stream_search(queries, Q, hist, N, d, k, p.s_chunk_rows, theta0, p.s_cap, cand, ccount, fl,

@@ -83,10 +83,10 @@ __device__ __forceinline__ void merge_query(uint64_t* slot, int q, const uint64_
 // and merges only the flagged queries.
 __global__ void __launch_bounds__(kMergeThreads) topk_merge_kernel(
     const uint64_t* __restrict__ partial, int Q, int n_lists, int list_len, int k, int per_group,
-    const int* __restrict__ only_flagged, const uint32_t* __restrict__ flag_word, uint32_t epoch,
+    const int* __restrict__ only_flagged, const uint32_t* __restrict__ flag_word,
     uint64_t* __restrict__ out_lists, int32_t* __restrict__ ids, float* __restrict__ sims) {
   __shared__ uint64_t slot[kMergeKeys];
-  if (only_flagged && *flag_word != epoch) return;
+  if (only_flagged && *flag_word == 0u) return;
   for (int q = blockIdx.x; q < Q; q += gridDim.x) {
     if (only_flagged && only_flagged[q] == 0) continue;
     __syncthreads();                            // the previous query's LDS reads are done
@@ -103,7 +103,6 @@ hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int li
   LaunchScope scope(only_flagged ? "topk_merge_fallback" : "topk_merge", stream);
   const int* flags = only_flagged ? only_flagged->flags : nullptr;
   const uint32_t* word = only_flagged ? only_flagged->word : nullptr;
-  const uint32_t epoch = only_flagged ? only_flagged->epoch : 0u;
   // One workgroup per query; as the fallback, at most 1024 that loop over the queries.
   const int gx = only_flagged ? std::min(Q, 1024) : Q;
   const int groups = merge_groups(Q, n_lists, list_len);
@@ -111,12 +110,12 @@ hipError_t launch_topk_merge(const uint64_t* partial, int Q, int n_lists, int li
     // Few queries with many lists: merge groups of lists in parallel first.
     const int per_group = (n_lists + groups - 1) / groups;
     hipLaunchKernelGGL(topk_merge_kernel, dim3(gx, groups), dim3(kMergeThreads), 0, stream, partial, Q,
-                       n_lists, list_len, k, per_group, flags, word, epoch, scratch_lists, nullptr, nullptr);
+                       n_lists, list_len, k, per_group, flags, word, scratch_lists, nullptr, nullptr);
     hipLaunchKernelGGL(topk_merge_kernel, dim3(gx), dim3(kMergeThreads), 0, stream, scratch_lists, Q, groups,
-                       list_len, k, groups, flags, word, epoch, nullptr, ids, sims);
+                       list_len, k, groups, flags, word, nullptr, ids, sims);
   } else {
     hipLaunchKernelGGL(topk_merge_kernel, dim3(gx), dim3(kMergeThreads), 0, stream, partial, Q, n_lists,
-                       list_len, k, n_lists, flags, word, epoch, nullptr, ids, sims);
+                       list_len, k, n_lists, flags, word, nullptr, ids, sims);
   }
   return hipGetLastError();
 }

@@ -73,17 +73,15 @@ hipError_t launch_stream_sample(EmbView queries, int Q, EmbView hist, int N, int
 // Test hook (sage_debug_theta_floor): a floor on the pre-pass threshold of the
 // filtered and stream paths; -inf when unset.
 float debug_theta_floor();
-// Queries sent to the exact fallback: flags[q] = 1 for each, and the
-// flagging kernel stores `epoch` (a value new to each call) in *word once any
-// query is flagged, so that the fallback kernels return at once when the word
-// holds another value. A stale word that matches costs time, never results:
-// the fallback still works from the flags.
+// Queries sent to the exact fallback: flags[q] = 1 for each, and *word = 1
+// once any query is flagged. The search's first kernel that always runs (the
+// filter kernel, the stream search) clears the word, so that the fallback
+// kernels return at once when it is still 0; nothing here depends on the
+// call, so a captured graph replays it as it stands.
 struct Flagged {
   int* flags;
   uint32_t* word;
-  uint32_t epoch;
 };
-uint32_t next_epoch();
 
 hipError_t launch_stream_search(EmbView queries, int Q, EmbView hist, int N, int d, int k, int chunk_rows,
                                 const float* theta0, int cap, uint64_t* cand, int* cand_count, Flagged fl,

@@ -167,10 +167,10 @@ def test_store_rejects_unsorted_bins():
 @pytest.mark.parametrize("Q,k", [(300, 32), (8, 64)])
 def test_fallback_word_from_an_earlier_call(Q, k):
     """One workspace for a call that flags queries (theta0 raised from the
-    host) and then for calls that flag none: the word the flagging call left
-    holds an older call's value, so the later calls' fallback launches return
-    at once, and their results equal the oracle's and the first unforced
-    call's bit for bit."""
+    host) and then for calls that flag none: the later calls clear the word
+    the flagging call set before their select runs, so their fallback
+    launches return at once, and their results equal the oracle's and the
+    first unforced call's bit for bit."""
     N, d = 60000, 64
     print(f"case Q={Q} k={k}", flush=True)
     w = workloads.small_predict(Q=Q, N=N, d=d, k=k, B=32, seed=900 + Q + k, clusters=5)
