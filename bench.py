@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also capture one step in a HIP graph and time its replays (modes 1-4)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
@@ -124,6 +126,30 @@ def timed_steps(step, steps: int, label: str, sage, torch, capacity: int = 64):
     stages = split.totals()
     split.close()
     return elapsed, dominant, stages
+
+
+def graph_replay(step, steps: int, rows: int, torch) -> dict:
+    """One step captured in a HIP graph (every launch on the capturing stream),
+    then `steps` replays timed on the wall clock: what a serving loop that
+    replays the decision pays per batch."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    return {"ms_per_step": 1e3 * elapsed / steps, "value": rows * steps / elapsed}
 
 
 def kernel_name(k: int, Q: int = 1 << 30) -> str:
@@ -260,9 +286,9 @@ def main():
     ws = torch.empty(max(16, sage.predict_workspace_bytes(Q, N, d, k, B)), dtype=torch.uint8, device="cuda")
     rws = torch.empty(max(16, sage.rank_workspace_bytes(Q)), dtype=torch.uint8, device="cuda")
     lib = sage.load_library()
-    stream = torch.cuda.current_stream().cuda_stream
 
     def step():
+        stream = torch.cuda.current_stream().cuda_stream
         sage._check(lib.sage_ingest_bf16_panels(queries_f32.data_ptr(), Q, d, qb.data_ptr(), stream))
         sage._check(lib.sage_predict_layout(qb.data_ptr(), PANELS, Q, hist.data_ptr(), PANELS,
                                             hist_len.data_ptr(), N, d, k, float(spec.tau),
@@ -318,6 +344,8 @@ def main():
                               ("topk_select", "select_kernel", ("k_sim_topk.hip", "sage_device.hpp"))):
         if stage in line["stage_rooflines"]:
             line["stage_rooflines"][stage]["traffic"] = read_traffic(kern, workload_key, srcs)
+    if args.graph:
+        line["graph_replay"] = graph_replay(step, args.steps, Q, torch)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)
@@ -387,6 +415,8 @@ def run_index_bound(args, torch, sage, workloads):
                              "achieved_GBs": att_bytes / att_s / 1e9,
                              "frac_of_hbm_peak": att_bytes / att_s / 1e9 / HBM_PEAK_GBS},
     }
+    if args.graph:
+        line["graph_replay"] = graph_replay(step, args.steps, Q, torch)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline_index(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)
